@@ -1,0 +1,294 @@
+// CPU oracle for the MoE dispatch/combine hot path.
+//
+// TEST INFRASTRUCTURE ONLY.  Nothing in the product path may call, link or
+// load this file's library; only the tests, the smoke check and the
+// benchmark's CPU-baseline leg do.  It shares no code, header, helper or
+// table with the HIP library: it is a plain, slow, single-threaded reading of
+// what the operator computes, written to be checked by eye against the paper.
+//
+// Built with: g++ -O2 -ffp-contract=off -shared -fPIC (see oracle/build.py).
+//
+// Notation (paper, Appendix D "Hierarchical Workload Partitioning for MoE
+// Dispatch/Combine"): each token t has k routed slots j with destination
+// expert e = topk_idx[t,j]; experts are spread over R peers ("ranks"), expert
+// e living on peer r = e / (E/R).  Token placement is the per-expert counts,
+// their prefix-sum offsets and each routed token's token-local offset inside
+// its expert window; expert windows of one peer are contiguous and form the
+// peer window whose payload is B_p.
+//
+// Readings where the paper is silent (each is listed in the design notes):
+//  * one routed row per (token, expert) pair, ordered by (expert, token);
+//  * slot value -1 marks an unused slot; an index outside [-1, E) and a
+//    repeat of an expert already chosen earlier in the same row are treated
+//    as unused and flagged in the status word (bits 1 and 2);
+//  * combine is the top-k-weighted sum of a token's expert outputs (the
+//    reduction of Section 6.1's reduction-bearing operators applied to the
+//    routed rows), evaluated here in double precision and rounded once to
+//    bf16 with round-to-nearest-even;
+//  * rows whose region-local index reaches the region capacity are neither
+//    written by dispatch nor read by combine, and set status bit 4.
+//
+// Parity pins for every function live in tests/test_oracle_*.py.
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+namespace {
+
+const uint32_t kBadIndex = 1u;   // index outside [-1, E)
+const uint32_t kDupIndex = 2u;   // expert repeated within one token's row
+const uint32_t kCapacity = 4u;   // region-local row >= region capacity
+
+}  // namespace
+
+extern "C" {
+
+// ---------------------------------------------------------------------------
+// Number formats.  Written from the IEEE-754 binary32 layout (bf16 is its
+// upper 16 bits: 1 sign, 8 exponent, 7 fraction bits) and from the OCP 8-bit
+// floating point specification (E4M3FN: bias 7, no infinities, S.1111.111 is
+// NaN, largest finite 448).
+// ---------------------------------------------------------------------------
+
+double oracle_bf16_to_double(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+// Round a double to the nearest bf16 value, ties to even, in one step.
+// bf16 keeps 8 significant bits and binary32's exponent range; below 2^-126
+// its spacing is fixed at 2^-133 (subnormals).
+uint16_t oracle_bf16_from_double(double x) {
+  uint16_t sign = std::signbit(x) ? 0x8000u : 0u;
+  if (std::isnan(x)) return (uint16_t)(sign | 0x7FC0u);
+  if (std::isinf(x)) return (uint16_t)(sign | 0x7F80u);
+  double ax = std::fabs(x);
+  if (ax == 0.0) return sign;
+  int e = std::ilogb(ax);                 // 2^e <= ax < 2^(e+1)
+  int q = (e < -126 ? -126 : e) - 7;      // exponent of one unit in the last place
+  double m = std::nearbyint(std::ldexp(ax, -q));  // exact scaling; ties-to-even
+  double r = std::ldexp(m, q);
+  if (r >= 0x1p128) return (uint16_t)(sign | 0x7F80u);  // overflow to infinity
+  float f = (float)r;                     // exact: r has <= 8 significant bits
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  return (uint16_t)(sign | (uint16_t)(u >> 16));
+}
+
+float oracle_fp8e4m3_to_float(uint8_t b) {
+  int s = b >> 7, ex = (b >> 3) & 0xF, m = b & 7;
+  if (ex == 15 && m == 7) return std::nanf("");
+  double v = ex == 0 ? std::ldexp((double)m, -9)               // m/8 * 2^(1-7)
+                     : std::ldexp(1.0 + m / 8.0, ex - 7);
+  return (float)(s ? -v : v);
+}
+
+// ---------------------------------------------------------------------------
+// Token placement (Appendix D, first and second level): per-expert and
+// per-peer counts, exclusive prefix-sum offsets, and a stable position for
+// every routed slot.  Plain counting sort keyed by expert, visiting tokens in
+// order, so rows of one expert window are in token order.
+//
+// Outputs: expert_count[E], expert_offset[E+1], rank_count[R],
+// rank_offset[R+1] (rank_offset[r] = expert_offset[r*E/R]), pos[T*k] (global
+// row of each slot, -1 if unused), row_src[T*k] (slot t*k+j of each global
+// row; -1 past the last row).  status |= bits.  Returns 0, or -1 on bad shape.
+// ---------------------------------------------------------------------------
+int oracle_layout(const int32_t* topk_idx, int64_t T, int32_t k, int32_t E,
+                  int32_t R, int32_t* expert_count, int32_t* expert_offset,
+                  int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
+                  int32_t* row_src, uint32_t* status) {
+  if (T < 0 || k < 1 || E < 1 || R < 1 || E % R != 0) return -1;
+  const int32_t L = E / R;
+  const int64_t S = T * k;
+  uint32_t st = 0;
+
+  // Which slots are routed.
+  std::vector<char> used((size_t)S, 0);
+  for (int64_t t = 0; t < T; ++t) {
+    for (int32_t j = 0; j < k; ++j) {
+      int32_t e = topk_idx[t * k + j];
+      if (e == -1) continue;
+      if (e < -1 || e >= E) { st |= kBadIndex; continue; }
+      bool repeat = false;
+      for (int32_t jj = 0; jj < j; ++jj)
+        if (topk_idx[t * k + jj] == e) repeat = true;
+      if (repeat) { st |= kDupIndex; continue; }
+      used[(size_t)(t * k + j)] = 1;
+    }
+  }
+
+  // Histogram over experts, then over peers.
+  for (int32_t e = 0; e < E; ++e) expert_count[e] = 0;
+  for (int64_t s = 0; s < S; ++s)
+    if (used[(size_t)s]) expert_count[topk_idx[s]] += 1;
+  for (int32_t r = 0; r < R; ++r) {
+    rank_count[r] = 0;
+    for (int32_t e = r * L; e < (r + 1) * L; ++e) rank_count[r] += expert_count[e];
+  }
+
+  // Exclusive prefix sums.
+  expert_offset[0] = 0;
+  for (int32_t e = 0; e < E; ++e) expert_offset[e + 1] = expert_offset[e] + expert_count[e];
+  for (int32_t r = 0; r < R; ++r) rank_offset[r] = expert_offset[r * L];
+  rank_offset[R] = expert_offset[E];
+
+  // Token-local offsets: the next free row of each expert window.
+  std::vector<int32_t> next(expert_offset, expert_offset + E);
+  for (int64_t s = 0; s < S; ++s) row_src[s] = -1;
+  for (int64_t t = 0; t < T; ++t) {
+    for (int32_t j = 0; j < k; ++j) {
+      int64_t s = t * k + j;
+      if (!used[(size_t)s]) { pos[s] = -1; continue; }
+      int32_t p = next[topk_idx[s]]++;
+      pos[s] = p;
+      row_src[p] = (int32_t)s;
+    }
+  }
+  *status |= st;
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Byte-balanced partition of the token range over P parts (Section 6.2 with a
+// single memory tier: every unit has the same cost model, the fan-out cap
+// does not bind, and a balanced split of the payload is what the list
+// scheduler reaches).  The cost of token t is 1 + (number of its routed
+// slots): one row read plus one row written per slot in dispatch, and the
+// mirror image in combine.  With a(t) the cost of tokens before t and A the
+// total, part p starts at bound[p] = the first t in [0, T] with
+// a(t) * P >= p * A, so part p holds the tokens whose cost prefix lies in
+// [p*A/P, (p+1)*A/P).  Output bound[P+1].
+// ---------------------------------------------------------------------------
+int oracle_plan(const int32_t* pos, int64_t T, int32_t k, int32_t P,
+                int32_t* bound) {
+  if (T < 0 || k < 1 || P < 1) return -1;
+  std::vector<int64_t> a((size_t)T + 1, 0);
+  for (int64_t t = 0; t < T; ++t) {
+    int64_t c = 1;
+    for (int32_t j = 0; j < k; ++j) c += pos[t * k + j] >= 0 ? 1 : 0;
+    a[(size_t)t + 1] = a[(size_t)t] + c;
+  }
+  const int64_t A = a[(size_t)T];
+  int64_t t = 0;
+  for (int64_t p = 0; p <= P; ++p) {
+    while (t < T && a[(size_t)t] * P < p * A) ++t;
+    bound[p] = (int32_t)t;
+  }
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Dispatch (Section 6.1 remote-slice transfers, one per routed slot: source
+// row t of x, destination peer r, destination row pos - rank_offset[r] of
+// that peer's receive region).  A pure byte copy of the row and, for fp8
+// payloads, of its row of block scales.  recv_x[r] / recv_s[r] are host
+// pointers to region r; recv_cap[r] is its capacity in rows.
+// ---------------------------------------------------------------------------
+int oracle_dispatch(const uint8_t* x, int64_t row_bytes, const uint8_t* x_scales,
+                    int64_t scale_row_bytes, int64_t T, int32_t k, int32_t E,
+                    int32_t R, const int32_t* topk_idx, const int32_t* pos,
+                    const int32_t* rank_offset, uint8_t* const* recv_x,
+                    uint8_t* const* recv_s, const int32_t* recv_cap,
+                    uint32_t* status) {
+  if (T < 0 || k < 1 || E < 1 || R < 1 || E % R != 0) return -1;
+  const int32_t L = E / R;
+  uint32_t st = 0;
+  for (int64_t t = 0; t < T; ++t) {
+    for (int32_t j = 0; j < k; ++j) {
+      int32_t p = pos[t * k + j];
+      if (p < 0) continue;
+      int32_t r = topk_idx[t * k + j] / L;
+      int64_t local = (int64_t)p - rank_offset[r];
+      if (local >= recv_cap[r]) { st |= kCapacity; continue; }
+      std::memcpy(recv_x[r] + local * row_bytes, x + t * row_bytes, (size_t)row_bytes);
+      if (x_scales)
+        std::memcpy(recv_s[r] + local * scale_row_bytes, x_scales + t * scale_row_bytes,
+                    (size_t)scale_row_bytes);
+    }
+  }
+  *status |= st;
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Stand-in expert used between dispatch and combine by the tests: expert e
+// multiplies its rows by s_e = 1 + 0.01*e (or 1 for the identity expert).
+// Computed in binary32 exactly as written -- s_e = 1.0f + (0.01f * e), bf16
+// input: v * s_e; fp8 input: (q * block_scale) * s_e, one rounding per
+// operation, no fused multiply-add -- then rounded to bf16 (nearest, ties to
+// even).  Region r holds rows of experts r*L .. r*L+L-1 in expert order;
+// expert_offset / rank_offset come from oracle_layout.
+// ---------------------------------------------------------------------------
+int oracle_expert_scale(uint8_t* const* recv_x, uint8_t* const* recv_s,
+                        int32_t payload_fp8, int32_t H, int32_t E, int32_t R,
+                        int32_t identity, const int32_t* expert_offset,
+                        const int32_t* rank_offset, const int32_t* recv_cap,
+                        uint16_t* const* out) {
+  if (H < 1 || E < 1 || R < 1 || E % R != 0) return -1;
+  const int32_t L = E / R;
+  const int32_t nblk = H / 128;
+  for (int32_t e = 0; e < E; ++e) {
+    const int32_t r = e / L;
+    const float se = identity ? 1.0f : 1.0f + 0.01f * (float)e;
+    for (int64_t g = expert_offset[e]; g < expert_offset[e + 1]; ++g) {
+      int64_t local = g - rank_offset[r];
+      if (local >= recv_cap[r]) continue;
+      uint16_t* o = out[r] + local * H;
+      for (int32_t h = 0; h < H; ++h) {
+        float v;
+        if (!payload_fp8) {
+          const uint16_t* in = (const uint16_t*)recv_x[r] + local * H;
+          v = (float)oracle_bf16_to_double(in[h]) * se;
+        } else {
+          const uint8_t* in = recv_x[r] + local * H;
+          float sc;
+          std::memcpy(&sc, recv_s[r] + (local * nblk + h / 128) * 4, 4);
+          float dq = oracle_fp8e4m3_to_float(in[h]) * sc;
+          v = dq * se;
+        }
+        o[h] = oracle_bf16_from_double((double)v);
+      }
+    }
+  }
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Combine: y[t] = sum over routed slots j of topk_w[t,j] * Y(row of slot j),
+// where Y is the bf16 expert-output region of the slot's peer at the same
+// region-local row dispatch wrote.  Sum in double, j ascending, then one
+// rounding to bf16.  A token with no routed slot gets y = +0.
+// ---------------------------------------------------------------------------
+int oracle_combine(uint16_t* const* expert_y, const float* topk_w, int64_t T,
+                   int32_t H, int32_t k, int32_t E, int32_t R,
+                   const int32_t* topk_idx, const int32_t* pos,
+                   const int32_t* rank_offset, const int32_t* recv_cap,
+                   uint16_t* y, uint32_t* status) {
+  if (T < 0 || H < 1 || k < 1 || E < 1 || R < 1 || E % R != 0) return -1;
+  const int32_t L = E / R;
+  uint32_t st = 0;
+  std::vector<double> acc((size_t)H);
+  for (int64_t t = 0; t < T; ++t) {
+    for (int32_t h = 0; h < H; ++h) acc[(size_t)h] = 0.0;
+    for (int32_t j = 0; j < k; ++j) {
+      int32_t p = pos[t * k + j];
+      if (p < 0) continue;
+      int32_t r = topk_idx[t * k + j] / L;
+      int64_t local = (int64_t)p - rank_offset[r];
+      if (local >= recv_cap[r]) { st |= kCapacity; continue; }
+      const uint16_t* row = expert_y[r] + local * H;
+      double w = (double)topk_w[t * k + j];
+      for (int32_t h = 0; h < H; ++h) acc[(size_t)h] += w * oracle_bf16_to_double(row[h]);
+    }
+    for (int32_t h = 0; h < H; ++h) y[t * H + h] = oracle_bf16_from_double(acc[(size_t)h]);
+  }
+  *status |= st;
+  return 0;
+}
+
+}  // extern "C"
