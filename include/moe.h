@@ -1,0 +1,201 @@
+/*
+ * moe.h -- C ABI of libmoe: the MoE dispatch/combine hot path on one MI355X.
+ *
+ * The operator follows the paper's MoE dispatch/combine (Section 8.1 and
+ * Table 2) and the hierarchical workload partitioning it is built on
+ * (Appendix D): token placement (per-expert counts, prefix-sum offsets and
+ * token-local offsets), expert windows grouped per peer into peer windows,
+ * and a byte-balanced split of the copy work over the GPU's workgroups
+ * (Section 6.2).  The R destination peers ("ranks") of expert parallelism are
+ * emulated as R separate receive regions in the same GPU's HBM, addressed
+ * through a device-side table of region base addresses; this table plays the
+ * role of the per-peer destination addresses of the remote-slice tuple
+ * <peer, src, dst, bytes, op, flag> of Section 6.1.
+ *
+ * Shapes and notation: T tokens, hidden size H, k routed slots per token,
+ * E experts spread over R ranks in contiguous blocks of L = E/R (expert e
+ * lives on rank e / L).  topk_idx[T,k] int32 holds the expert of each slot
+ * (-1 = unused slot), topk_w[T,k] float32 its combine weight.  One routed row
+ * exists per (token, expert) pair; rows are ordered by (expert, token), so
+ * the rows of rank r are the global rows [rank_offset[r], rank_offset[r+1])
+ * and land in region r at region-local row (global row - rank_offset[r]).
+ *
+ * Conventions for every entry point:
+ *  - All array arguments are DEVICE pointers unless marked "host".  The
+ *    caller allocates and owns every buffer; the library allocates, frees
+ *    and caches no memory.  It keeps no state between calls other than the
+ *    device properties it reads once per device.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Every call only enqueues kernels on `stream` and returns without
+ *    synchronizing; outputs are ready when the stream reaches that point.
+ *  - Return codes (host side, checked before anything is enqueued; on error
+ *    nothing is launched): MOE_OK, MOE_EINVAL (null pointer where one is
+ *    required, T < 0, k < 1, k > MOE_MAX_K, k > E, E % R != 0,
+ *    E > MOE_MAX_EXPERTS, T*k > INT32_MAX, H < 1, bad dtype), MOE_EALIGN (x,
+ *    region or y base not 16-byte aligned, row bytes not a multiple of 16,
+ *    fp8 H not a multiple of 128, scale pointers not 4-byte aligned),
+ *    MOE_EWORKSPACE (workspace too small or not 256-byte aligned),
+ *    MOE_ELAUNCH (a HIP launch failed; moe_last_hip_error() has the code).
+ *  - Device status word `status` (uint32, device): the caller zeroes it;
+ *    kernels OR these bits into it and the caller reads it whenever it
+ *    synchronizes: MOE_STATUS_BAD_INDEX (an index outside [-1, E): the slot
+ *    is treated as unused), MOE_STATUS_DUP_INDEX (an expert repeated within
+ *    one token's row: later repeats are treated as unused),
+ *    MOE_STATUS_CAPACITY (a row's region-local index is outside
+ *    [0, recv_cap[r]): dispatch does not write it and combine does not read
+ *    it; a negative index only arises when pos does not belong to topk_idx).
+ *  - The three calls of one batch must see the same topk_idx, T, k, E, R and
+ *    workspace; dispatch and combine read the partition plan that moe_layout
+ *    leaves in the workspace.
+ */
+#ifndef MOE_H_
+#define MOE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_VERSION 1
+
+#define MOE_OK 0
+#define MOE_EINVAL (-1)
+#define MOE_EALIGN (-2)
+#define MOE_EWORKSPACE (-3)
+#define MOE_ELAUNCH (-4)
+
+#define MOE_DTYPE_BF16 0     /* hidden rows of H bf16 values (2H bytes) */
+#define MOE_DTYPE_FP8_E4M3 1 /* H OCP E4M3FN bytes + H/128 float32 block scales */
+
+#define MOE_STATUS_BAD_INDEX 1u
+#define MOE_STATUS_DUP_INDEX 2u
+#define MOE_STATUS_CAPACITY 4u
+
+#define MOE_MAX_K 32
+#define MOE_MAX_EXPERTS 1024
+#define MOE_FP8_BLOCK 128
+
+/* Number of parts of the byte-balanced partition plan.  One wavefront of
+ * moe_dispatch and of moe_combine handles one part. */
+#define MOE_PLAN_PARTS 4096
+
+/* Library version (MOE_VERSION). */
+int moe_version(void);
+
+/* Static, human-readable text for a return code. */
+const char* moe_strerror(int code);
+
+/* The hipError_t of the last failed launch on the calling thread (0 if
+ * none). */
+int moe_last_hip_error(void);
+
+/*
+ * moe_layout_workspace_bytes -- device workspace that moe_layout needs for
+ * a batch of this shape (written to *out_bytes, a HOST pointer).  The
+ * workspace starts with the partition plan: int32 bound[MOE_PLAN_PARTS + 1],
+ * token boundaries of the parts (part p = tokens [bound[p], bound[p+1])).
+ * The rest is scratch whose content is internal.
+ */
+int moe_layout_workspace_bytes(int64_t T, int k, int E, int R, size_t* out_bytes);
+
+/*
+ * moe_layout -- token placement (Appendix D, first level: destination
+ * expert, per-expert counts, prefix-sum offsets and token-local offsets;
+ * second and third level: expert windows and the peer windows they form)
+ * plus the byte-balanced partition plan (Section 6.2, one memory tier).
+ *
+ * In:  topk_idx [T,k] int32 row-major.
+ * Out: expert_count[E]      routed slots per expert;
+ *      expert_offset[E+1]   exclusive prefix sum of expert_count
+ *                           (expert_offset[E] = number of routed slots N);
+ *      rank_count[R]        routed slots per rank (peer window sizes, rows);
+ *      rank_offset[R+1]     rank_offset[r] = expert_offset[r*L], [R] = N;
+ *      pos[T*k]             global row of slot (t,j), -1 if unused: rows are
+ *                           ordered by (expert, token), so
+ *                           pos = expert_offset[e] + #{t' < t routed to e};
+ *      row_src[T*k]         inverse map: slot index t*k+j of global row i for
+ *                           i < N, -1 for i >= N;
+ *      workspace            partition plan (see above) + scratch;
+ *      status               OR-ed bits (BAD_INDEX, DUP_INDEX).
+ * Results are deterministic and bit-identical from run to run.  T = 0 is
+ * allowed (counts and offsets become 0).
+ */
+int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
+               int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
+               int32_t* rank_offset, int32_t* pos, int32_t* row_src, void* workspace,
+               size_t workspace_bytes, uint32_t* status, void* stream);
+
+/*
+ * moe_dispatch -- copy every routed token row to its destination rank's
+ * receive region (Section 6.1 remote-slice transfers with op = store, one
+ * per routed slot; work split over wavefronts by bytes, Section 6.2 and
+ * Appendix D third level).  A pure byte copy: for each routed slot (t,j)
+ * with expert e, rank r = e/L and local = pos[t*k+j] - rank_offset[r] <
+ * recv_cap[r]:
+ *      region_r[local, :] = x[t, :]                       (row_bytes)
+ *      scale_region_r[local, :] = x_scales[t, :]          (fp8 only)
+ *
+ * x         [T,H] bf16 (dtype BF16) or [T,H] E4M3FN bytes (dtype FP8_E4M3),
+ *           16-byte aligned; row bytes = 2H or H, a multiple of 16.
+ * x_scales  [T,H/128] float32 for FP8_E4M3, else NULL.
+ * recv_x    [R] uint64 region base addresses (device table), 16-byte aligned;
+ *           region r holds recv_cap[r] rows of row_bytes each.
+ * recv_scales [R] uint64 scale-region bases (FP8_E4M3) or NULL; region r
+ *           holds recv_cap[r] rows of (H/128)*4 bytes, 4-byte aligned.
+ * recv_cap  [R] int32 capacity of each region in rows.
+ * topk_idx, pos, rank_offset, workspace: as produced by moe_layout.
+ * Bytes of a region beyond the rows dispatch writes are left untouched.
+ */
+int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H,
+                 int k, int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                 const int32_t* rank_offset, const uint64_t* recv_x,
+                 const uint64_t* recv_scales, const int32_t* recv_cap,
+                 const void* workspace, size_t workspace_bytes, uint32_t* status,
+                 void* stream);
+
+/*
+ * moe_combine -- gather each token's expert outputs back to token order and
+ * reduce them with the top-k weights (Section 6.1: operands are loaded and
+ * accumulated on chip, then written once; token-centric, so no two
+ * wavefronts write the same output row and no atomics are needed):
+ *      y[t, :] = bf16( sum over routed slots j of topk_w[t,j] * Y_r[local, :] )
+ * with r, local as in moe_dispatch and Y_r the bf16 expert-output region of
+ * rank r (expert_y[r], rows of 2H bytes).  Products and the sum are float32,
+ * the result is rounded to bf16 to nearest-even.  A token with no routed
+ * slot gets +0.  Slots whose local row reaches recv_cap[r] are skipped.
+ *
+ * expert_y  [R] uint64 bf16 region bases (device table), 16-byte aligned.
+ * topk_w    [T,k] float32.
+ * y         [T,H] bf16 output, 16-byte aligned, 2H a multiple of 16.
+ */
+int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
+                int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
+                const void* workspace, size_t workspace_bytes, uint32_t* status,
+                void* stream);
+
+/*
+ * moe_expert_scale -- stand-in expert for tests and benchmarks, not part of
+ * the operator: for every global row g < expert_offset[E] of expert e on
+ * rank r with local = g - rank_offset[r] < recv_cap[r],
+ *      out_r[local, h] = bf16( v * s_e ),  s_e = identity ? 1 : 1 + 0.01*e
+ * where v = float(bf16 input) or (float(fp8 input) * block scale), every
+ * step a separately rounded float32 operation (no fused multiply-add) and
+ * the result rounded to bf16 to nearest-even.
+ *
+ * recv_x / recv_scales: region tables as for moe_dispatch (dtype selects the
+ * payload); out_y: [R] uint64 bf16 output regions (rows of 2H bytes).
+ * max_rows: an upper bound on expert_offset[E] (normally T*k).
+ */
+int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int dtype, int H,
+                     int E, int R, int identity, const int32_t* expert_offset,
+                     const int32_t* rank_offset, const int32_t* recv_cap,
+                     const uint64_t* out_y, int64_t max_rows, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H_ */

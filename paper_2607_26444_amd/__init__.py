@@ -1,0 +1,10 @@
+"""MoE dispatch/combine hot path for one MI355X (gfx950).
+
+The operator itself is the C ABI in include/moe.h, implemented by the HIP
+kernels under csrc/ and built into libmoe.so; `moe` is its ctypes binding.
+"""
+from .moe import (  # noqa: F401
+    EXPORTS, MOE_DTYPE_BF16, MOE_DTYPE_FP8_E4M3, MOE_PLAN_PARTS, MOE_STATUS_BAD_INDEX,
+    MOE_STATUS_CAPACITY, MOE_STATUS_DUP_INDEX, Layout, MoeError, Regions, lib,
+    moe_combine, moe_dispatch, moe_expert_scale, moe_layout, moe_layout_workspace_bytes,
+    moe_version)

@@ -1,0 +1,165 @@
+// C ABI of libmoe (declared in include/moe.h): argument validation and
+// kernel launches.  Nothing here allocates, frees or synchronizes.
+
+#include <limits.h>
+
+#include "moe_internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int shape_ok(int64_t T, int k, int E, int R) {
+  if (T < 0 || k < 1 || k > MOE_MAX_K || E < 1 || E > MOE_MAX_EXPERTS || R < 1 || k > E ||
+      E % R != 0)
+    return MOE_EINVAL;
+  if (T > 0 && T > (int64_t)INT32_MAX / k) return MOE_EINVAL;
+  return MOE_OK;
+}
+
+int launched(hipError_t err) {
+  if (err == hipSuccess) return MOE_OK;
+  g_last_hip_error = (int)err;
+  return MOE_ELAUNCH;
+}
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+int moe_version(void) { return MOE_VERSION; }
+
+const char* moe_strerror(int code) {
+  switch (code) {
+    case MOE_OK: return "ok";
+    case MOE_EINVAL: return "invalid argument (null pointer or unsupported shape)";
+    case MOE_EALIGN: return "misaligned pointer or row size";
+    case MOE_EWORKSPACE: return "workspace too small or misaligned";
+    case MOE_ELAUNCH: return "HIP kernel launch failed";
+    default: return "unknown error";
+  }
+}
+
+int moe_last_hip_error(void) { return g_last_hip_error; }
+
+int moe_layout_workspace_bytes(int64_t T, int k, int E, int R, size_t* out_bytes) {
+  if (!out_bytes) return MOE_EINVAL;
+  const int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  *out_bytes = moe::layout_geom(T, E).total;
+  return MOE_OK;
+}
+
+int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R, int32_t* expert_count,
+               int32_t* expert_offset, int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
+               int32_t* row_src, void* workspace, size_t workspace_bytes, uint32_t* status,
+               void* stream) {
+  int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  if (!expert_count || !expert_offset || !rank_count || !rank_offset || !workspace || !status)
+    return MOE_EINVAL;
+  if (T > 0 && (!topk_idx || !pos || !row_src)) return MOE_EINVAL;
+  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
+    return MOE_EWORKSPACE;
+  return launched(moe::launch_layout(topk_idx, T, k, E, R, expert_count, expert_offset,
+                                     rank_count, rank_offset, pos, row_src, workspace, status,
+                                     as_stream(stream)));
+}
+
+int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k, int E,
+                 int R, const int32_t* topk_idx, const int32_t* pos, const int32_t* rank_offset,
+                 const uint64_t* recv_x, const uint64_t* recv_scales, const int32_t* recv_cap,
+                 const void* workspace, size_t workspace_bytes, uint32_t* status,
+                 void* stream) {
+  int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  if (H < 1 || (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3)) return MOE_EINVAL;
+  const bool fp8 = dtype == MOE_DTYPE_FP8_E4M3;
+  if (!recv_x || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
+  if (fp8 && (!x_scales || !recv_scales)) return MOE_EINVAL;
+  if (T > 0 && (!x || !topk_idx || !pos)) return MOE_EINVAL;
+  const int64_t row_bytes = fp8 ? (int64_t)H : 2 * (int64_t)H;
+  if (row_bytes % 16 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
+  if (!aligned(x, 16) || (fp8 && !aligned(x_scales, 4))) return MOE_EALIGN;
+  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
+    return MOE_EWORKSPACE;
+  if (T == 0) return MOE_OK;
+  moe::DispatchArgs a;
+  a.x = static_cast<const uint8_t*>(x);
+  a.x_scales = fp8 ? reinterpret_cast<const uint8_t*>(x_scales) : nullptr;
+  a.row_bytes = row_bytes;
+  a.scale_row_bytes = fp8 ? (H / MOE_FP8_BLOCK) * 4 : 0;
+  a.k = k;
+  a.L = E / R;
+  a.topk_idx = topk_idx;
+  a.pos = pos;
+  a.rank_offset = rank_offset;
+  a.recv_x = recv_x;
+  a.recv_scales = fp8 ? recv_scales : nullptr;
+  a.recv_cap = recv_cap;
+  a.bound = static_cast<const int32_t*>(workspace);
+  a.status = status;
+  return launched(moe::launch_dispatch(a, as_stream(stream)));
+}
+
+int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k, int E,
+                int R, const int32_t* topk_idx, const int32_t* pos, const int32_t* rank_offset,
+                const int32_t* recv_cap, uint16_t* y, const void* workspace,
+                size_t workspace_bytes, uint32_t* status, void* stream) {
+  int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  if (H < 1) return MOE_EINVAL;
+  if (!expert_y || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
+  if (T > 0 && (!topk_w || !topk_idx || !pos || !y)) return MOE_EINVAL;
+  if ((2 * (int64_t)H) % 16 != 0 || !aligned(y, 16)) return MOE_EALIGN;
+  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
+    return MOE_EWORKSPACE;
+  if (T == 0) return MOE_OK;
+  moe::CombineArgs a;
+  a.expert_y = expert_y;
+  a.topk_w = topk_w;
+  a.row_bytes = 2 * (int64_t)H;
+  a.k = k;
+  a.L = E / R;
+  a.topk_idx = topk_idx;
+  a.pos = pos;
+  a.rank_offset = rank_offset;
+  a.recv_cap = recv_cap;
+  a.y = y;
+  a.bound = static_cast<const int32_t*>(workspace);
+  a.status = status;
+  return launched(moe::launch_combine(a, as_stream(stream)));
+}
+
+int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int dtype, int H,
+                     int E, int R, int identity, const int32_t* expert_offset,
+                     const int32_t* rank_offset, const int32_t* recv_cap, const uint64_t* out_y,
+                     int64_t max_rows, void* stream) {
+  if (H < 1 || E < 1 || E > MOE_MAX_EXPERTS || R < 1 || E % R != 0 || max_rows < 0)
+    return MOE_EINVAL;
+  if (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3) return MOE_EINVAL;
+  const bool fp8 = dtype == MOE_DTYPE_FP8_E4M3;
+  if (!recv_x || !expert_offset || !rank_offset || !recv_cap || !out_y) return MOE_EINVAL;
+  if (fp8 && !recv_scales) return MOE_EINVAL;
+  if (H % 8 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
+  if (max_rows == 0) return MOE_OK;
+  moe::ExpertArgs a;
+  a.recv_x = recv_x;
+  a.recv_scales = fp8 ? recv_scales : nullptr;
+  a.H = H;
+  a.E = E;
+  a.L = E / R;
+  a.identity = identity;
+  a.expert_offset = expert_offset;
+  a.rank_offset = rank_offset;
+  a.recv_cap = recv_cap;
+  a.out_y = out_y;
+  a.max_rows = max_rows;
+  return launched(moe::launch_expert_scale(a, fp8, as_stream(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,142 @@
+// Dispatch: copy each routed token row into its rank's receive region.
+//
+// Work split (Section 6.2 with one memory tier, Appendix D third level):
+// moe_layout leaves MOE_PLAN_PARTS contiguous token ranges of equal byte
+// cost (a token costs one row read plus one row write per routed slot).  One
+// wavefront takes one part, so every wavefront moves the same number of
+// bytes no matter how skewed the routing is; a hot expert only changes where
+// rows land, not who copies them.
+//
+// Push direction: a wavefront reads its token's row from x once into
+// registers (16 bytes per lane per 1 KiB segment, so a 14 KiB row is 14
+// dwordx4 loads in flight per lane) and stores it to each of the token's k
+// destinations.  x is read exactly once; every destination row is written
+// by exactly one wavefront with full 1 KiB coalesced stores.  Slot metadata
+// (pos, expert, region base, capacity) for a batch of 64/k tokens is loaded
+// once, one slot per lane, before any row moves; the copy loop then takes
+// each destination from its lane with readlane, so no load of metadata sits
+// between row stores.
+
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+// VPL: 1 KiB segments held per lane-set (row bytes up to VPL KiB per pass).
+// FULL: row bytes == VPL KiB exactly (no per-lane tail test).
+template <int VPL, bool FULL, bool SCALES>
+__global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int part = uniform(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+  if (part >= MOE_PLAN_PARTS) return;
+  const int t0 = a.bound[part], t1 = a.bound[part + 1];
+  const int64_t rb = a.row_bytes;
+  const int sb = a.scale_row_bytes;
+  const int k = a.k;
+  const int tpb = kWave / k;        // tokens whose slots fit one lane each
+  const int lt = lane / k;          // this lane's token within a batch
+  const int lj = lane - lt * k;     // ... and its slot
+  uint32_t st = 0;
+
+  for (int tb = t0; tb < t1; tb += tpb) {
+    const int te = min(t1, tb + tpb);
+    // Destination of slot (tb + lt, lj), resolved once per batch by its lane.
+    uint64_t dst = 0, sdst = 0;
+    bool ok = false;
+    if (tb + lt < te) {
+      const int64_t s = (int64_t)(tb + lt) * k + lj;
+      const int p = a.pos[s];
+      if (p >= 0) {
+        const int r = a.topk_idx[s] / a.L;
+        const int local = p - a.rank_offset[r];
+        if (local >= 0 && local < a.recv_cap[r]) {
+          dst = a.recv_x[r] + (uint64_t)local * (uint64_t)rb;
+          if (SCALES) sdst = a.recv_scales[r] + (uint64_t)local * (uint64_t)sb;
+          ok = true;
+        } else {
+          st |= MOE_STATUS_CAPACITY;
+        }
+      }
+    }
+    const uint64_t okm = __ballot(ok);
+
+    for (int t = tb; t < te; ++t) {
+      const int l0 = (t - tb) * k;
+      const uint8_t* src = a.x + (int64_t)t * rb;
+      for (int64_t seg = 0; seg < rb; seg += VPL * kWaveBytes) {
+        u32x4 v[VPL];
+#pragma unroll
+        for (int c = 0; c < VPL; ++c) {
+          const int64_t off = seg + c * kWaveBytes + lane * kVecBytes;
+          if (FULL || off < rb) v[c] = ld16(src + off);
+        }
+        for (int j = 0; j < k; ++j) {
+          if (!((okm >> (l0 + j)) & 1ull)) continue;
+          uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(dst, l0 + j));
+#pragma unroll
+          for (int c = 0; c < VPL; ++c) {
+            const int64_t off = seg + c * kWaveBytes + lane * kVecBytes;
+            if (FULL || off < rb) st16(d + off, v[c]);
+          }
+        }
+      }
+      if (SCALES) {
+        // Block scales, one float32 per lane per pass.
+        const uint8_t* ssrc = a.x_scales + (int64_t)t * sb;
+        for (int o = 0; o < sb; o += kWave * 4) {
+          const int off = o + lane * 4;
+          uint32_t sv = 0;
+          if (off < sb) sv = ld4(ssrc + off);
+          for (int j = 0; j < k; ++j) {
+            if (!((okm >> (l0 + j)) & 1ull)) continue;
+            uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(sdst, l0 + j));
+            if (off < sb) st4(d + off, sv);
+          }
+        }
+      }
+    }
+  }
+  st = wave_or(st);
+  if (st && lane == 0) atomicOr(a.status, st);
+}
+
+template <int VPL, bool SCALES>
+hipError_t launch_vpl(const DispatchArgs& a, hipStream_t stream) {
+  const dim3 grid(MOE_PLAN_PARTS / kWavesPerBlock), block(kBlock);
+  if (a.row_bytes == (int64_t)VPL * kWaveBytes)
+    hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((dispatch_kernel<VPL, false, SCALES>), grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+template <bool SCALES>
+hipError_t launch_scales(const DispatchArgs& a, hipStream_t stream) {
+  const int64_t segs = (a.row_bytes + kWaveBytes - 1) / kWaveBytes;
+  switch (segs) {
+    case 1: return launch_vpl<1, SCALES>(a, stream);
+    case 2: return launch_vpl<2, SCALES>(a, stream);
+    case 3: return launch_vpl<3, SCALES>(a, stream);
+    case 4: return launch_vpl<4, SCALES>(a, stream);
+    case 5: return launch_vpl<5, SCALES>(a, stream);
+    case 6: return launch_vpl<6, SCALES>(a, stream);
+    case 7: return launch_vpl<7, SCALES>(a, stream);
+    case 8: return launch_vpl<8, SCALES>(a, stream);
+    case 9: return launch_vpl<9, SCALES>(a, stream);
+    case 10: return launch_vpl<10, SCALES>(a, stream);
+    case 11: return launch_vpl<11, SCALES>(a, stream);
+    case 12: return launch_vpl<12, SCALES>(a, stream);
+    case 13: return launch_vpl<13, SCALES>(a, stream);
+    case 14: return launch_vpl<14, SCALES>(a, stream);
+    case 15: return launch_vpl<15, SCALES>(a, stream);
+    default: return launch_vpl<kMaxSegVecs, SCALES>(a, stream);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t stream) {
+  return a.x_scales ? launch_scales<true>(a, stream) : launch_scales<false>(a, stream);
+}
+
+}  // namespace moe

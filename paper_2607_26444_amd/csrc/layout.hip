@@ -1,0 +1,337 @@
+// Token placement and partition plan (paper Appendix D, first to third
+// level; Section 6.2 for the byte-balanced split).
+//
+// Two kernels, both one workgroup per chunk of tokens:
+//
+//   layout_count  per-chunk expert histogram.  Each wavefront owns 64
+//                 consecutive tokens (one per lane) and sets, for every
+//                 routed slot, bit `lane` of an LDS bitmap mask[wave][e]
+//                 (ds_or_b64).  The chunk's count for expert e is the sum of
+//                 the popcounts of its four wavefront bitmaps.  Bitmap ORs do
+//                 not serialize on a hot expert the way counter atomics do,
+//                 and the result does not depend on arrival order.
+//
+//   layout_place  every chunk reads the whole [nc][E] count matrix (small by
+//                 construction), derives the global per-expert totals, their
+//                 exclusive scan (expert_offset) and its own column prefix,
+//                 then rebuilds its bitmaps and gives each routed slot
+//                     pos = expert_offset[e] + (rows of e in earlier chunks)
+//                         + (rows of e in earlier sub-chunks of this chunk)
+//                         + popcount(bits of e in earlier wavefronts)
+//                         + popcount(mask[wave][e] & lanes below this lane).
+//                 Since a token routes to an expert at most once, this is the
+//                 stable (expert, token) order.  The same pass scans the
+//                 per-token cost 1 + (routed slots) and writes the partition
+//                 boundaries that fall inside the chunk.
+//
+// Both kernels decide slot validity with the same routine (load_row), so
+// counts and positions always agree.
+
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+// Load token t's k expert indices and decide which slots are routed: an
+// index in [0, E) that does not repeat an earlier slot of the row.
+template <int KW>
+__device__ __forceinline__ void load_row(const int32_t* __restrict__ idx, int64_t t, int64_t T,
+                                         int k, int E, int (&ev)[KW], bool (&ok)[KW],
+                                         uint32_t& st) {
+#pragma unroll
+  for (int j = 0; j < KW; ++j) ev[j] = -1;
+  if (t < T) {
+#pragma unroll
+    for (int j = 0; j < KW; ++j)
+      if (j < k) ev[j] = idx[t * k + j];
+  }
+#pragma unroll
+  for (int j = 0; j < KW; ++j) {
+    const int e = ev[j];
+    const bool in_range = e >= 0 && e < E;
+    if (e < -1 || e >= E) st |= MOE_STATUS_BAD_INDEX;
+    bool repeat = false;
+#pragma unroll
+    for (int jj = 0; jj < j; ++jj) repeat |= (ev[jj] == e);
+    if (in_range && repeat) st |= MOE_STATUS_DUP_INDEX;
+    ok[j] = in_range && !repeat;
+  }
+}
+
+// Exclusive scan of one int64 per thread over the 256-thread block; also
+// returns the block total.  `scratch` holds kWavesPerBlock int64.
+__device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* scratch,
+                                                        int64_t& total) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  int64_t inc = v;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t o = __shfl_up(inc, d, kWave);
+    if (lane >= d) inc += o;
+  }
+  if (lane == kWave - 1) scratch[w] = inc;
+  __syncthreads();
+  int64_t before = 0;
+  total = 0;
+#pragma unroll
+  for (int i = 0; i < kWavesPerBlock; ++i) {
+    const int64_t s = scratch[i];
+    before += (i < w) ? s : 0;
+    total += s;
+  }
+  __syncthreads();
+  return before + inc - v;
+}
+
+template <int KW>
+__global__ __launch_bounds__(kBlock) void layout_count_kernel(
+    const int32_t* __restrict__ idx, int64_t T, int k, int E, int64_t chunk_tokens,
+    int32_t* __restrict__ counts, uint32_t* __restrict__ status) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint64_t* mask = reinterpret_cast<uint64_t*>(smem);           // [4][E]
+  int32_t* cnt = reinterpret_cast<int32_t*>(mask + kWavesPerBlock * E);  // [E]
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int64_t c0 = (int64_t)blockIdx.x * chunk_tokens;
+  const int64_t c1 = min(T, c0 + chunk_tokens);
+
+  for (int i = tid; i < kWavesPerBlock * E; i += kBlock) mask[i] = 0;
+  for (int e = tid; e < E; e += kBlock) cnt[e] = 0;
+  uint32_t st = 0;
+  __syncthreads();
+
+  for (int64_t s0 = c0; s0 < c1; s0 += kBlock) {
+    int ev[KW];
+    bool ok[KW];
+    load_row<KW>(idx, s0 + tid, c1, k, E, ev, ok, st);
+#pragma unroll
+    for (int j = 0; j < KW; ++j)
+      if (ok[j]) atomicOr(&mask[w * E + ev[j]], 1ull << lane);
+    __syncthreads();
+    for (int e = tid; e < E; e += kBlock) {
+      int c = 0;
+#pragma unroll
+      for (int q = 0; q < kWavesPerBlock; ++q) {
+        c += __popcll(mask[q * E + e]);
+        mask[q * E + e] = 0;
+      }
+      cnt[e] += c;
+    }
+    __syncthreads();
+  }
+  for (int e = tid; e < E; e += kBlock) counts[(int64_t)blockIdx.x * E + e] = cnt[e];
+  st = wave_or(st);
+  if (lane == 0 && st) atomicOr(status, st);
+}
+
+constexpr int kMaxExpertsPerThread = MOE_MAX_EXPERTS / kBlock;  // 4
+
+template <int KW>
+__global__ __launch_bounds__(kBlock) void layout_place_kernel(
+    const int32_t* __restrict__ idx, int64_t T, int k, int E, int R, int64_t chunk_tokens,
+    int nc, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
+    int32_t* __restrict__ expert_offset, int32_t* __restrict__ rank_count,
+    int32_t* __restrict__ rank_offset, int32_t* __restrict__ pos,
+    int32_t* __restrict__ row_src, int32_t* __restrict__ bound) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint64_t* mask = reinterpret_cast<uint64_t*>(smem);               // [4][E]
+  int64_t* scan = reinterpret_cast<int64_t*>(mask + kWavesPerBlock * E);  // [4]
+  int32_t* base = reinterpret_cast<int32_t*>(scan + kWavesPerBlock);  // [E]
+  int32_t* eoff = base + E;                                         // [E+1]
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int c = blockIdx.x;
+  const int64_t c0 = (int64_t)c * chunk_tokens;
+  const int64_t c1 = min(T, c0 + chunk_tokens);
+  const int P = MOE_PLAN_PARTS;
+
+  for (int i = tid; i < kWavesPerBlock * E; i += kBlock) mask[i] = 0;
+
+  // Totals and this chunk's prefix for the experts this thread owns:
+  // e = tid*EPT .. tid*EPT+EPT-1 (contiguous, so a scan over threads is a
+  // scan over experts).
+  const int ept = (E + kBlock - 1) / kBlock;
+  int tot[kMaxExpertsPerThread], pre[kMaxExpertsPerThread];
+#pragma unroll
+  for (int q = 0; q < kMaxExpertsPerThread; ++q) tot[q] = pre[q] = 0;
+  for (int cc = 0; cc < nc; ++cc) {
+    const int32_t* row = counts + (int64_t)cc * E;
+#pragma unroll
+    for (int q = 0; q < kMaxExpertsPerThread; ++q) {
+      const int e = tid * ept + q;
+      if (q < ept && e < E) {
+        const int v = row[e];
+        tot[q] += v;
+        pre[q] += (cc < c) ? v : 0;
+      }
+    }
+  }
+  int64_t my_tot = 0, my_pre = 0;
+#pragma unroll
+  for (int q = 0; q < kMaxExpertsPerThread; ++q) {
+    my_tot += tot[q];
+    my_pre += pre[q];
+  }
+  int64_t n_total = 0;
+  int64_t run = block_exclusive_scan(my_tot, scan, n_total);  // rows before my experts
+  int64_t pre_total = 0;
+  (void)block_exclusive_scan(my_pre, scan, pre_total);         // routed slots before chunk
+#pragma unroll
+  for (int q = 0; q < kMaxExpertsPerThread; ++q) {
+    const int e = tid * ept + q;
+    if (q < ept && e < E) {
+      eoff[e] = (int32_t)run;
+      base[e] = (int32_t)(run + pre[q]);
+      if (c == 0) {
+        expert_count[e] = tot[q];
+        expert_offset[e] = (int32_t)run;
+      }
+      run += tot[q];
+    }
+  }
+  if (tid == 0) eoff[E] = (int32_t)n_total;
+  __syncthreads();
+  if (c == 0) {
+    const int L = E / R;
+    if (tid == 0) {
+      expert_offset[E] = (int32_t)n_total;
+      rank_offset[R] = (int32_t)n_total;
+      bound[0] = 0;
+    }
+    for (int r = tid; r < R; r += kBlock) {
+      rank_offset[r] = eoff[r * L];
+      rank_count[r] = eoff[(r + 1) * L] - eoff[r * L];
+    }
+    if (T == 0)
+      for (int p = tid; p <= P; p += kBlock) bound[p] = 0;
+  }
+
+  // Partition plan: token cost 1 + routed slots, total A = T + N.
+  const int64_t A = T + n_total;
+  int64_t cost_base = c0 + pre_total;
+
+  uint32_t st_unused = 0;
+  for (int64_t s0 = c0; s0 < c1; s0 += kBlock) {
+    const int64_t t = s0 + tid;
+    int ev[KW];
+    bool ok[KW];
+    load_row<KW>(idx, t, c1, k, E, ev, ok, st_unused);
+    int nvalid = 0;
+#pragma unroll
+    for (int j = 0; j < KW; ++j)
+      if (ok[j]) {
+        atomicOr(&mask[w * E + ev[j]], 1ull << lane);
+        ++nvalid;
+      }
+    __syncthreads();
+    const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int j = 0; j < KW; ++j) {
+      if (t < c1 && j < k) {
+        int p = -1;
+        if (ok[j]) {
+          const int e = ev[j];
+          int r = base[e] + __popcll(mask[w * E + e] & below);
+          for (int q = 0; q < w; ++q) r += __popcll(mask[q * E + e]);
+          p = r;
+          row_src[p] = (int32_t)(t * k + j);
+        }
+        pos[t * k + j] = p;
+      }
+    }
+    // Plan boundaries inside this sub-chunk: token t owns the parts p with
+    // a_t*P < p*A <= (a_t + cost_t)*P, each starting at token t+1.
+    const int64_t cost = (t < c1) ? 1 + nvalid : 0;
+    int64_t sub_total = 0;
+    const int64_t a = cost_base + block_exclusive_scan(cost, scan, sub_total);
+    if (cost) {
+      const int64_t p_lo = (a * P) / A + 1, p_hi = ((a + cost) * P) / A;
+      for (int64_t p = p_lo; p <= p_hi; ++p) bound[p] = (int32_t)(t + 1);
+    }
+    cost_base += sub_total;
+    __syncthreads();
+    for (int e = tid; e < E; e += kBlock) {
+      int n = 0;
+#pragma unroll
+      for (int q = 0; q < kWavesPerBlock; ++q) {
+        n += __popcll(mask[q * E + e]);
+        mask[q * E + e] = 0;
+      }
+      base[e] += n;
+    }
+    __syncthreads();
+  }
+
+  // Rows past the last routed slot have no source.
+  for (int64_t i = n_total + (int64_t)c * kBlock + tid; i < T * k; i += (int64_t)nc * kBlock)
+    row_src[i] = -1;
+}
+
+template <int KW>
+hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
+                            int32_t* expert_count, int32_t* expert_offset,
+                            int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
+                            int32_t* row_src, void* workspace, uint32_t* status,
+                            hipStream_t stream) {
+  const LayoutGeom g = layout_geom(T, E);
+  int32_t* bound = reinterpret_cast<int32_t*>(workspace);
+  int32_t* counts = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + g.plan_bytes);
+  const size_t lds_count = (size_t)kWavesPerBlock * E * 8 + (size_t)E * 4;
+  const size_t lds_place = (size_t)kWavesPerBlock * E * 8 + kWavesPerBlock * 8 +
+                           (size_t)E * 4 + (size_t)(E + 1) * 4;
+  hipLaunchKernelGGL(layout_count_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_count, stream,
+                     idx, T, k, E, g.chunk_tokens, counts, status);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(layout_place_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_place, stream,
+                     idx, T, k, E, R, g.chunk_tokens, g.nc, counts, expert_count,
+                     expert_offset, rank_count, rank_offset, pos, row_src, bound);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+LayoutGeom layout_geom(int64_t T, int E) {
+  // At most max(1, 32768/E) chunks, each a multiple of kBlock tokens.
+  const int64_t nc_max = E >= 32768 ? 1 : 32768 / E;
+  const int64_t per = (T + kBlock * nc_max - 1) / (kBlock * nc_max);
+  LayoutGeom g;
+  g.chunk_tokens = kBlock * (per < 1 ? 1 : per);
+  g.nc = (int)((T + g.chunk_tokens - 1) / g.chunk_tokens);
+  if (g.nc < 1) g.nc = 1;
+  g.plan_bytes = ((size_t)(MOE_PLAN_PARTS + 1) * 4 + 255) / 256 * 256;
+  g.counts_bytes = (size_t)g.nc * E * 4;
+  g.total = g.plan_bytes + (g.counts_bytes + 255) / 256 * 256;
+  return g;
+}
+
+int slot_width(int k) {
+  int kw = 2;
+  while (kw < k) kw *= 2;
+  return kw;
+}
+
+hipError_t launch_layout(const int32_t* idx, int64_t T, int k, int E, int R,
+                         int32_t* expert_count, int32_t* expert_offset,
+                         int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
+                         int32_t* row_src, void* workspace, uint32_t* status,
+                         hipStream_t stream) {
+  switch (slot_width(k)) {
+    case 2:
+      return launch_layout_kw<2>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
+                                 rank_offset, pos, row_src, workspace, status, stream);
+    case 4:
+      return launch_layout_kw<4>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
+                                 rank_offset, pos, row_src, workspace, status, stream);
+    case 8:
+      return launch_layout_kw<8>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
+                                 rank_offset, pos, row_src, workspace, status, stream);
+    case 16:
+      return launch_layout_kw<16>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
+                                  rank_offset, pos, row_src, workspace, status, stream);
+    default:
+      return launch_layout_kw<32>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
+                                  rank_offset, pos, row_src, workspace, status, stream);
+  }
+}
+
+}  // namespace moe

@@ -1,0 +1,144 @@
+// Internal declarations of libmoe (HIP, gfx950).  Kernels live in
+// layout.hip, dispatch.hip, combine.hip and expert.hip; api.hip validates
+// arguments and calls the launchers declared here.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "moe.h"
+
+namespace moe {
+
+constexpr int kWave = 64;            // CDNA wavefront width
+constexpr int kBlock = 256;          // threads per workgroup (4 wavefronts)
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kVecBytes = 16;        // one dwordx4 per lane
+constexpr int kWaveBytes = kWave * kVecBytes;  // 1 KiB per wavefront access
+constexpr int kMaxSegVecs = 16;      // a wavefront holds up to 16 KiB of a row
+
+// Geometry of the layout pass: tokens are cut into nc chunks of chunk_tokens
+// (a multiple of kBlock); each chunk is one workgroup.  The chunk count is
+// bounded so that the per-chunk expert count matrix [nc][E] stays small
+// enough for every placement workgroup to read all of it.
+struct LayoutGeom {
+  int64_t chunk_tokens;
+  int nc;
+  size_t plan_bytes;    // bound[MOE_PLAN_PARTS + 1], padded to 256 bytes
+  size_t counts_bytes;  // int32 [nc][E]
+  size_t total;
+};
+
+LayoutGeom layout_geom(int64_t T, int E);
+
+// Slot width the layout kernels are compiled for: smallest of 2, 4, 8, 16,
+// 32 that is >= k.
+int slot_width(int k);
+
+hipError_t launch_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
+                         int32_t* expert_count, int32_t* expert_offset,
+                         int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
+                         int32_t* row_src, void* workspace, uint32_t* status,
+                         hipStream_t stream);
+
+struct DispatchArgs {
+  const uint8_t* x;
+  const uint8_t* x_scales;     // nullptr for bf16 payloads
+  int64_t row_bytes;           // 2H (bf16) or H (fp8)
+  int32_t scale_row_bytes;     // (H/128)*4 or 0
+  int32_t k;
+  int32_t L;                   // experts per rank
+  const int32_t* topk_idx;
+  const int32_t* pos;
+  const int32_t* rank_offset;
+  const uint64_t* recv_x;
+  const uint64_t* recv_scales;
+  const int32_t* recv_cap;
+  const int32_t* bound;        // plan: bound[MOE_PLAN_PARTS + 1]
+  uint32_t* status;
+};
+
+hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t stream);
+
+struct CombineArgs {
+  const uint64_t* expert_y;
+  const float* topk_w;
+  int64_t row_bytes;           // 2H
+  int32_t k;
+  int32_t L;
+  const int32_t* topk_idx;
+  const int32_t* pos;
+  const int32_t* rank_offset;
+  const int32_t* recv_cap;
+  uint16_t* y;
+  const int32_t* bound;
+  uint32_t* status;
+};
+
+hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+
+struct ExpertArgs {
+  const uint64_t* recv_x;
+  const uint64_t* recv_scales;
+  int32_t H;
+  int32_t E;
+  int32_t L;
+  int32_t identity;
+  const int32_t* expert_offset;
+  const int32_t* rank_offset;
+  const int32_t* recv_cap;
+  const uint64_t* out_y;
+  int64_t max_rows;
+};
+
+hipError_t launch_expert_scale(const ExpertArgs& a, bool fp8, hipStream_t stream);
+
+// ---------------------------------------------------------------- device
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) u32x4 gu32x4;
+typedef __attribute__((address_space(1))) uint32_t gu32;
+
+// 16-byte and 4-byte accesses to global memory.  Addresses built from
+// integers (region tables, readlane) would otherwise compile to flat
+// instructions, which also count against the scalar/LDS wait counter.
+__device__ __forceinline__ u32x4 ld16(const void* p) {
+  return *(const gu32x4*)(uintptr_t)p;
+}
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *(gu32x4*)(uintptr_t)p = v; }
+__device__ __forceinline__ uint32_t ld4(const void* p) { return *(const gu32*)(uintptr_t)p; }
+__device__ __forceinline__ void st4(void* p, uint32_t v) { *(gu32*)(uintptr_t)p = v; }
+
+// Wavefront-uniform value held in a scalar register.
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Value of lane `l` (wavefront-uniform l) of a 64-bit per-lane value.
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ float readlane_f32(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v |= __shfl_xor(v, d, kWave);
+  return v;
+}
+
+// bf16 <-> float32.  bf16 is the upper half of a binary32 pattern; the
+// float -> bf16 direction uses gfx950's conversion, which rounds to nearest
+// even.
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+}  // namespace moe

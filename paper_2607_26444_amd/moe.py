@@ -1,0 +1,207 @@
+"""ctypes binding of libmoe (include/moe.h).
+
+Argument marshalling only: every function passes device pointers of torch
+tensors and the current HIP stream to the C entry point of the same name;
+all work runs in the library's kernels.  torch is imported before the
+library is loaded so that both use the one HIP runtime already in the
+process.  There is no fallback: without libmoe.so every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmoe.so")
+
+MOE_OK = 0
+MOE_EINVAL = -1
+MOE_EALIGN = -2
+MOE_EWORKSPACE = -3
+MOE_ELAUNCH = -4
+
+MOE_DTYPE_BF16 = 0
+MOE_DTYPE_FP8_E4M3 = 1
+
+MOE_STATUS_BAD_INDEX = 1
+MOE_STATUS_DUP_INDEX = 2
+MOE_STATUS_CAPACITY = 4
+
+MOE_MAX_K = 32
+MOE_MAX_EXPERTS = 1024
+MOE_FP8_BLOCK = 128
+MOE_PLAN_PARTS = 4096
+
+# Entry points declared in include/moe.h.
+EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error",
+           "moe_layout_workspace_bytes", "moe_layout", "moe_dispatch",
+           "moe_combine", "moe_expert_scale")
+
+_lib = None
+P = ctypes.c_void_p
+I32 = ctypes.c_int
+I64 = ctypes.c_int64
+SZ = ctypes.c_size_t
+
+
+class MoeError(RuntimeError):
+    def __init__(self, fn, code):
+        msg = lib().moe_strerror(code).decode()
+        if code == MOE_ELAUNCH:
+            msg += f" (hipError {lib().moe_last_hip_error()})"
+        super().__init__(f"{fn}: {msg} [{code}]")
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2607_26444_amd.build` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.moe_version.restype = I32
+        L.moe_strerror.argtypes = [I32]
+        L.moe_strerror.restype = ctypes.c_char_p
+        L.moe_last_hip_error.restype = I32
+        L.moe_layout_workspace_bytes.argtypes = [I64, I32, I32, I32, ctypes.POINTER(SZ)]
+        L.moe_layout.argtypes = [P, I64, I32, I32, I32, P, P, P, P, P, P, P, SZ, P, P]
+        L.moe_dispatch.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, P,
+                                   P, SZ, P, P]
+        L.moe_combine.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P, P]
+        L.moe_expert_scale.argtypes = [P, P, I32, I32, I32, I32, I32, P, P, P, P, I64, P]
+        for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_dispatch",
+                  "moe_combine", "moe_expert_scale"):
+            getattr(L, f).restype = I32
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("libmoe takes device tensors only")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(fn, rc):
+    if rc != MOE_OK:
+        raise MoeError(fn, rc)
+
+
+def moe_version() -> int:
+    return lib().moe_version()
+
+
+def moe_layout_workspace_bytes(T: int, k: int, E: int, R: int) -> int:
+    out = SZ(0)
+    _check("moe_layout_workspace_bytes",
+           lib().moe_layout_workspace_bytes(T, k, E, R, ctypes.byref(out)))
+    return out.value
+
+
+def moe_layout(topk_idx, E, R, expert_count, expert_offset, rank_count, rank_offset,
+               pos, row_src, workspace, status, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_layout", lib().moe_layout(
+        _ptr(topk_idx), T, k, E, R, _ptr(expert_count), _ptr(expert_offset),
+        _ptr(rank_count), _ptr(rank_offset), _ptr(pos), _ptr(row_src), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(status), _stream(stream)))
+
+
+def moe_dispatch(x, x_scales, dtype, H, E, R, topk_idx, pos, rank_offset, recv_x,
+                 recv_scales, recv_cap, workspace, status, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_dispatch", lib().moe_dispatch(
+        _ptr(x), _ptr(x_scales), dtype, T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
+        _ptr(rank_offset), _ptr(recv_x), _ptr(recv_scales), _ptr(recv_cap),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(status),
+        _stream(stream)))
+
+
+def moe_combine(expert_y, topk_w, H, E, R, topk_idx, pos, rank_offset, recv_cap, y,
+                workspace, status, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_combine", lib().moe_combine(
+        _ptr(expert_y), _ptr(topk_w), T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
+        _ptr(rank_offset), _ptr(recv_cap), _ptr(y), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(status), _stream(stream)))
+
+
+def moe_expert_scale(recv_x, recv_scales, dtype, H, E, R, identity, expert_offset,
+                     rank_offset, recv_cap, out_y, max_rows, stream=None):
+    _check("moe_expert_scale", lib().moe_expert_scale(
+        _ptr(recv_x), _ptr(recv_scales), dtype, H, E, R, int(bool(identity)),
+        _ptr(expert_offset), _ptr(rank_offset), _ptr(recv_cap), _ptr(out_y), max_rows,
+        _stream(stream)))
+
+
+# ------------------------------------------------------------ buffer plumbing
+class Layout:
+    """Device outputs of moe_layout for one batch shape."""
+
+    def __init__(self, T, k, E, R, device="cuda"):
+        i32 = dict(dtype=torch.int32, device=device)
+        self.T, self.k, self.E, self.R = T, k, E, R
+        self.expert_count = torch.empty(E, **i32)
+        self.expert_offset = torch.empty(E + 1, **i32)
+        self.rank_count = torch.empty(R, **i32)
+        self.rank_offset = torch.empty(R + 1, **i32)
+        self.pos = torch.empty(max(1, T * k), **i32)
+        self.row_src = torch.empty(max(1, T * k), **i32)
+        nbytes = moe_layout_workspace_bytes(T, k, E, R)
+        # torch's caching allocator returns 512-byte aligned blocks
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        assert self.workspace.data_ptr() % 256 == 0
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def run(self, topk_idx, stream=None):
+        moe_layout(topk_idx, self.E, self.R, self.expert_count, self.expert_offset,
+                   self.rank_count, self.rank_offset, self.pos, self.row_src,
+                   self.workspace, self.status, stream)
+
+    def plan(self):
+        """The partition plan bound[MOE_PLAN_PARTS + 1] (a view of the workspace)."""
+        return self.workspace[: (MOE_PLAN_PARTS + 1) * 4].view(torch.int32)
+
+
+class Regions:
+    """R receive regions carved from one allocation, each 4 KiB aligned, with
+    a device table of their base addresses (the emulated ranks)."""
+
+    ALIGN = 4096
+
+    def __init__(self, rows, row_bytes, device="cuda", guard_bytes=0, fill=None):
+        self.rows = [int(r) for r in rows]
+        self.row_bytes = int(row_bytes)
+        self.guard = int(guard_bytes)
+        offs, cur = [], self.guard
+        for n in self.rows:
+            cur = (cur + self.ALIGN - 1) // self.ALIGN * self.ALIGN
+            offs.append(cur)
+            cur += n * self.row_bytes + self.guard
+        total = (cur + self.ALIGN - 1) // self.ALIGN * self.ALIGN + self.ALIGN
+        self.buf = torch.empty(total, dtype=torch.uint8, device=device)
+        if fill is not None:
+            self.buf.fill_(fill)
+        base = self.buf.data_ptr()
+        pad = (-base) % self.ALIGN
+        self.offsets = [o + pad for o in offs]
+        self.table = torch.tensor([base + o for o in self.offsets], dtype=torch.int64,
+                                  device=device)
+        self.cap = torch.tensor(self.rows, dtype=torch.int32, device=device)
+
+    def region(self, r):
+        o = self.offsets[r]
+        return self.buf[o: o + self.rows[r] * self.row_bytes].view(
+            self.rows[r], self.row_bytes)

@@ -1,0 +1,179 @@
+"""Run the HIP path end to end through the C ABI and the oracle beside it.
+
+Used by the GPU parity tests and the smoke check.  Inputs come from
+`workloads`; the oracle chain (layout -> dispatch -> expert -> combine) is
+computed from the same inputs only, never from GPU results.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+import workloads as wl
+from paper_2607_26444_amd import moe
+
+SENTINEL = 0xA5
+GUARD = 4096
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a: np.ndarray) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to("cuda")
+
+
+def u8_rows(a: np.ndarray) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    return a.view(np.uint8).reshape(a.shape[0], -1)
+
+
+class GpuRun:
+    """One pass of layout -> dispatch -> expert -> combine on the GPU."""
+
+    def __init__(self, cfg, inp, topk_idx=None, topk_w=None, spare_rows=0,
+                 cap_delta=None, identity=None, combine_on_dispatch=False):
+        self.cfg = cfg
+        T, H, E, R = cfg["T"], cfg["H"], cfg["E"], cfg["R"]
+        idx = inp["topk_idx"] if topk_idx is None else topk_idx
+        w = inp["topk_w"] if topk_w is None else topk_w
+        k = idx.shape[1]
+        fp8 = cfg["payload"] == wl.FP8_E4M3
+        dtype = moe.MOE_DTYPE_FP8_E4M3 if fp8 else moe.MOE_DTYPE_BF16
+        ident = (cfg["expert"] == "identity") if identity is None else identity
+        self.idx, self.w, self.k = idx, w, k
+
+        idx_d = to_dev(idx.astype(np.int32))
+        w_d = to_dev(w.astype(np.float32))
+        lay = moe.Layout(T, k, E, R)
+        lay.run(idx_d)
+        torch.cuda.synchronize()
+        counts = lay.rank_count.cpu().numpy()
+        caps = counts.astype(np.int64) + spare_rows
+        if cap_delta is not None:
+            caps = np.maximum(0, caps + np.asarray(cap_delta))
+        self.caps = caps.astype(np.int32)
+        rows = [int(c) for c in self.caps]
+
+        rb, sb = wl.row_bytes(cfg), wl.scale_row_bytes(cfg)
+        self.regions = moe.Regions(rows, rb, guard_bytes=GUARD, fill=SENTINEL)
+        cap_d = to_dev(self.caps)
+        self.sregions = None
+        x_d = to_dev(u8_rows(inp["x"]))
+        xs_d = None
+        if fp8:
+            self.sregions = moe.Regions(rows, sb, guard_bytes=GUARD, fill=SENTINEL)
+            xs_d = to_dev(inp["x_scales"]).view(torch.float32)
+        moe.moe_dispatch(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                         self.regions.table, self.sregions.table if fp8 else None,
+                         cap_d, lay.workspace, lay.status)
+
+        y = torch.empty((max(1, T), H), dtype=torch.int16, device="cuda")
+        y.fill_(0x5A5A)
+        if combine_on_dispatch:
+            assert not fp8
+            ey_table = self.regions.table
+            self.eregions = None
+        else:
+            self.eregions = moe.Regions(rows, 2 * H, guard_bytes=GUARD, fill=SENTINEL)
+            moe.moe_expert_scale(self.regions.table,
+                                 self.sregions.table if fp8 else None, dtype, H, E, R,
+                                 ident, lay.expert_offset, lay.rank_offset, cap_d,
+                                 self.eregions.table, max(1, T * k))
+            ey_table = self.eregions.table
+        moe.moe_combine(ey_table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, cap_d,
+                        y, lay.workspace, lay.status)
+        torch.cuda.synchronize()
+
+        self.layout = dict(
+            expert_count=lay.expert_count.cpu().numpy(),
+            expert_offset=lay.expert_offset.cpu().numpy(),
+            rank_count=counts,
+            rank_offset=lay.rank_offset.cpu().numpy(),
+            pos=lay.pos.cpu().numpy()[: T * k],
+            row_src=lay.row_src.cpu().numpy()[: T * k],
+            status=int(lay.status.cpu().numpy()[0]))
+        self.plan = lay.plan().cpu().numpy()
+        self.y = y.cpu().numpy().view(np.uint16)[:T]
+        self._lay = lay
+
+    def region_bytes(self, regions):
+        return regions.buf.cpu().numpy(), regions.offsets
+
+
+def oracle_chain(cfg, inp, topk_idx=None, topk_w=None, caps=None, identity=None,
+                 combine_on_dispatch=False):
+    E, R, H = cfg["E"], cfg["R"], cfg["H"]
+    idx = inp["topk_idx"] if topk_idx is None else topk_idx
+    w = inp["topk_w"] if topk_w is None else topk_w
+    fp8 = cfg["payload"] == wl.FP8_E4M3
+    ident = (cfg["expert"] == "identity") if identity is None else identity
+    lay = oracle.layout(idx, E, R)
+    cap = lay["rank_count"] if caps is None else caps
+    xs = u8_rows(inp["x_scales"]) if fp8 else None
+    regs, sregs, st_d = oracle.dispatch(u8_rows(inp["x"]), xs, idx, lay["pos"],
+                                        lay["rank_offset"], E, R, cap, SENTINEL)
+    if combine_on_dispatch:
+        ey = [r.view(np.uint16).reshape(r.shape[0], H) for r in regs]
+    else:
+        ey = oracle.expert_scale(regs, sregs, fp8, H, E, R, ident, lay["expert_offset"],
+                                 lay["rank_offset"], cap)
+    y, st_c = oracle.combine(ey, w, idx, lay["pos"], lay["rank_offset"], cap, E, R, H)
+    return dict(layout=lay, regs=regs, sregs=sregs, ey=ey, y=y, status=st_d | st_c)
+
+
+def bf16_to_f64(a):
+    return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def combine_close(y, y_ref, rtol=8e-3, atol=1e-3):
+    """|y - y_ref| <= rtol*|y_ref| + atol, element-wise (NaN must match)."""
+    a, b = bf16_to_f64(y), bf16_to_f64(y_ref)
+    nan = np.isnan(b)
+    if not np.array_equal(np.isnan(a), nan):
+        return False, "NaN mismatch"
+    err = np.abs(a[~nan] - b[~nan])
+    bound = rtol * np.abs(b[~nan]) + atol
+    bad = err > bound
+    if bad.any():
+        i = int(np.argmax(err - bound))
+        return False, f"{int(bad.sum())} elements out of tolerance; worst err {err[i]} " \
+                      f"bound {bound[i]}"
+    return True, f"max err/bound {float((err / bound).max()) if err.size else 0:.3f}"
+
+
+def check_regions(run, regions, oracle_regs, rows_written=None):
+    """Region bytes equal the oracle's (only the first rows_written[r] rows of
+    region r when given; the rest must keep the sentinel); guard bands and
+    gaps between regions keep the sentinel."""
+    buf = regions.buf.cpu().numpy()
+    mask = np.ones(buf.shape[0], bool)
+    for r, off in enumerate(regions.offsets):
+        n_cap = regions.rows[r]
+        got = buf[off: off + n_cap * regions.row_bytes].reshape(n_cap, regions.row_bytes)
+        want = oracle_regs[r]
+        if rows_written is not None:
+            n = int(rows_written[r])
+            assert np.all(got[n:] == SENTINEL), f"region {r}: rows past {n} written"
+            got, want = got[:n], want[:n]
+        assert got.shape == want.shape, (r, got.shape, want.shape)
+        if not np.array_equal(got, want):
+            bad = np.nonzero((got != want).any(1))[0]
+            raise AssertionError(f"region {r}: {len(bad)} rows differ, first {bad[:5]}")
+        mask[off: off + n_cap * regions.row_bytes] = False
+    outside = buf[mask]
+    assert np.all(outside == SENTINEL), "bytes outside the regions were written"
+
+
+def f32_bits_to_bf16_rne(f32: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of float32 values via torch's CPU cast (RNE)."""
+    t = torch.from_numpy(np.ascontiguousarray(f32, np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
