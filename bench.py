@@ -1,0 +1,276 @@
+"""Benchmark of the MoE dispatch/combine hot path on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                [--no-cpu-baseline]
+
+One step = one pass of the whole path on one batch already resident in HBM:
+moe_layout (histograms, scans, placement, partition plan) -> moe_dispatch
+(rows into R emulated rank regions) -> moe_combine (top-k weighted gather).
+The stand-in expert between dispatch and combine is run once before timing
+(it is not part of the operator); combine reads its outputs every step.
+
+Prints one JSON line.  `value` is dispatch+combine algorithmic bytes per
+second of whole-step time (the layout's time is included, its bytes are
+not credited).  Algorithmic bytes: dispatch reads x once and writes every
+routed row plus 4 bytes of pos per slot; combine reads every routed row
+plus 8 bytes (weight, pos) per slot and writes y.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+
+
+def algorithmic_bytes(cfg) -> dict:
+    T, H, k = cfg["T"], cfg["H"], cfg["k"]
+    fp8 = cfg["payload"] == 1
+    row = H * (1 if fp8 else 2) + ((H // 128) * 4 if fp8 else 0)
+    n = T * k
+    dispatch = T * row + n * row + 4 * n
+    combine = n * 2 * H + 8 * n + T * 2 * H
+    return dict(dispatch=dispatch, combine=combine, row=row, n=n)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_26444_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            a, b = line.split(":", 1)
+            kv[a.strip()] = b.strip()
+    if kv.get("source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(cfg, inp, budget_s=12.0, max_reps=3):
+    """The CPU oracle (single-threaded) on the same workload: layout, dispatch
+    and combine, timed on this host.  Its combine reads the dispatched rows
+    directly (identity expert); the cost does not depend on the values."""
+    import oracle
+    E, R, H = cfg["E"], cfg["R"], cfg["H"]
+    fp8 = cfg["payload"] == 1
+    x_rows = np.ascontiguousarray(inp["x"]).view(np.uint8).reshape(cfg["T"], -1)
+    xs_rows = (np.ascontiguousarray(inp["x_scales"]).view(np.uint8).reshape(cfg["T"], -1)
+               if fp8 else None)
+    times = []
+    t_start = time.perf_counter()
+    for _ in range(max_reps):
+        t0 = time.perf_counter()
+        lay = oracle.layout(inp["topk_idx"], E, R)
+        t1 = time.perf_counter()
+        regs, _, _ = oracle.dispatch(x_rows, xs_rows, inp["topk_idx"], lay["pos"],
+                                     lay["rank_offset"], E, R, lay["rank_count"])
+        t2 = time.perf_counter()
+        if fp8:
+            ey = [np.zeros((r.shape[0], H), np.uint16) for r in regs]
+        else:
+            ey = [r.view(np.uint16).reshape(r.shape[0], H) for r in regs]
+        t3 = time.perf_counter()
+        oracle.combine(ey, inp["topk_w"], inp["topk_idx"], lay["pos"], lay["rank_offset"],
+                       lay["rank_count"], E, R, H)
+        t4 = time.perf_counter()
+        times.append((t1 - t0) + (t2 - t1) + (t4 - t3))
+        del regs, ey
+        if time.perf_counter() - t_start > budget_s:
+            break
+    return float(np.median(times)), len(times)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="prefill")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    a = ap.parse_args(argv)
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU's share of the operator; runs on more than "
+              "one GPU are not part of this build (use --gpus 1).", file=sys.stderr)
+        return 2
+
+    import torch
+    import workloads as wl
+    from paper_2607_26444_amd import moe
+
+    cfg = wl.get(a.workload)
+    T, H, E, R, k = cfg["T"], cfg["H"], cfg["E"], cfg["R"], cfg["k"]
+    fp8 = cfg["payload"] == wl.FP8_E4M3
+    dtype = moe.MOE_DTYPE_FP8_E4M3 if fp8 else moe.MOE_DTYPE_BF16
+    print(f"[bench] workload {cfg['name']}: generating inputs", file=sys.stderr, flush=True)
+    inp = wl.make_inputs(cfg)
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    x_d = torch.from_numpy(np.ascontiguousarray(inp["x"]).view(np.uint8)).to(dev)
+    xs_d = torch.from_numpy(inp["x_scales"]).to(dev) if fp8 else None
+    idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
+    w_d = torch.from_numpy(inp["topk_w"]).to(dev)
+
+    lay = moe.Layout(T, k, E, R)
+    lay.run(idx_d)
+    torch.cuda.synchronize()
+    counts = lay.rank_count.cpu().numpy()
+    rows = [max(1, int(c)) for c in counts]
+    rb, sb = wl.row_bytes(cfg), wl.scale_row_bytes(cfg)
+    regions = moe.Regions(rows, rb)
+    sregions = moe.Regions(rows, sb) if fp8 else None
+    eregions = moe.Regions(rows, 2 * H)
+    y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+
+    def dispatch():
+        moe.moe_dispatch(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                         regions.table, sregions.table if fp8 else None, regions.cap,
+                         lay.workspace, lay.status)
+
+    def combine():
+        moe.moe_combine(eregions.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                        eregions.cap, y, lay.workspace, lay.status)
+
+    # stand-in expert outputs for combine (once, untimed)
+    dispatch()
+    moe.moe_expert_scale(regions.table, sregions.table if fp8 else None, dtype, H, E, R,
+                         cfg["expert"] == "identity", lay.expert_offset, lay.rank_offset,
+                         regions.cap, eregions.table, T * k)
+    torch.cuda.synchronize()
+
+    for _ in range(a.warmup):
+        lay.run(idx_d)
+        dispatch()
+        combine()
+    torch.cuda.synchronize()
+    status = int(lay.status.item())
+    if status != 0:
+        print(f"[bench] status word {status} after warmup", file=sys.stderr)
+        return 1
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
+    print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(a.steps):
+        ev[s][0].record(stream)
+        lay.run(idx_d)
+        ev[s][1].record(stream)
+        dispatch()
+        ev[s][2].record(stream)
+        combine()
+        ev[s][3].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    lay_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    dis_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    com_ms = np.array([e[2].elapsed_time(e[3]) for e in ev])
+    step_ms = wall * 1e3 / a.steps
+    b = algorithmic_bytes(cfg)
+    dc_bytes = b["dispatch"] + b["combine"]
+    value = dc_bytes / (step_ms * 1e-3) / 1e9
+    d_us, c_us, l_us = dis_ms.mean() * 1e3, com_ms.mean() * 1e3, lay_ms.mean() * 1e3
+    d_gbps = b["dispatch"] / (d_us * 1e-6) / 1e9
+    c_gbps = b["combine"] / (c_us * 1e-6) / 1e9
+    dom = "dispatch" if d_us >= c_us else "combine"
+    dom_bytes, dom_us = (b["dispatch"], d_us) if dom == "dispatch" else (b["combine"], c_us)
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
+    traffic = read_traffic(cfg["name"], dom)
+
+    out = {
+        "metric": "dispatch+combine effective GB/s (algorithmic bytes / whole-step time)",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8_e4m3+f32" if fp8 else "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "T": T, "H": H, "E": E, "R": R, "k": k,
+                   "payload": "fp8_e4m3" if fp8 else "bf16", "zipf_s": cfg["zipf_s"],
+                   "force_frac": cfg["force_frac"], "parallelism": "1 GPU, R emulated ranks"},
+        "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "tokens_per_s": round(T / (step_ms * 1e-3), 1),
+        "layout_us": round(l_us, 2),
+        "dispatch_us": round(d_us, 2),
+        "combine_us": round(c_us, 2),
+        "dispatch_GBps": round(d_gbps, 1),
+        "combine_GBps": round(c_gbps, 1),
+        "dispatch_plus_combine_GBps": round(dc_bytes / ((d_us + c_us) * 1e-6) / 1e9, 1),
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic},
+        "cpu_baseline": None,
+    }
+    # Achievable-bandwidth reference on the same GPU: a plain device copy of
+    # 1 GiB (read + write bytes / time), next to the 8 TB/s peak.
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    out["hbm_copy_GBps"] = round(2 * src.numel() * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del src, dst
+
+    if not a.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        cpu_s, reps = cpu_baseline(cfg, inp)
+        out["cpu_baseline"] = {
+            "value": round(dc_bytes / cpu_s / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"full workload (layout+dispatch+combine), median of {reps} run(s), "
+                      f"{cpu_s:.2f} s each, 1 thread, host CPU: {cpu_model()}",
+            "tokens_per_s": round(T / cpu_s, 1)}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -31,9 +31,10 @@
  *  - Return codes (host side, checked before anything is enqueued; on error
  *    nothing is launched): MOE_OK, MOE_EINVAL (null pointer where one is
  *    required, T < 0, k < 1, k > MOE_MAX_K, k > E, E % R != 0,
- *    E > MOE_MAX_EXPERTS, T*k > INT32_MAX, H < 1, bad dtype), MOE_EALIGN (x,
- *    region or y base not 16-byte aligned, row bytes not a multiple of 16,
- *    fp8 H not a multiple of 128, scale pointers not 4-byte aligned),
+ *    E > MOE_MAX_EXPERTS, T*k > INT32_MAX, H < 1, bad dtype), MOE_EALIGN (x
+ *    or y not 16-byte aligned, row bytes not a multiple of 16, fp8 H not a
+ *    multiple of 128, x_scales not 4-byte aligned; region base addresses sit
+ *    in device tables and their alignment is the caller's to keep),
  *    MOE_EWORKSPACE (workspace too small or not 256-byte aligned),
  *    MOE_ELAUNCH (a HIP launch failed; moe_last_hip_error() has the code).
  *  - Device status word `status` (uint32, device): the caller zeroes it;
@@ -77,9 +78,12 @@ extern "C" {
 #define MOE_MAX_EXPERTS 1024
 #define MOE_FP8_BLOCK 128
 
-/* Number of parts of the byte-balanced partition plan.  One wavefront of
- * moe_dispatch and of moe_combine handles one part. */
-#define MOE_PLAN_PARTS 4096
+/* Number of parts of the byte-balanced partition plan.  moe_dispatch and
+ * moe_combine launch W wavefronts, W the number the GPU keeps resident for
+ * the kernel (rounded down to a divisor of MOE_PLAN_PARTS), and wavefront g
+ * takes the contiguous parts [g*P/W, (g+1)*P/W).  12288 = 3 * 2^12 divides
+ * evenly over 256 compute units at 4, 8, 12, 16, 24 or 48 wavefronts each. */
+#define MOE_PLAN_PARTS 12288
 
 /* Library version (MOE_VERSION). */
 int moe_version(void);

@@ -3,7 +3,38 @@
 
 #include <limits.h>
 
+#include <map>
+#include <mutex>
+#include <utility>
+
 #include "moe_internal.h"
+
+namespace moe {
+
+int resident_waves(const void* kernel, size_t lds_bytes) {
+  static std::mutex mu;
+  static std::map<std::pair<int, const void*>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find({dev, kernel});
+  if (it != cache.end()) return it->second;
+  int cus = 0, blocks = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, kBlock, lds_bytes) !=
+          hipSuccess ||
+      cus < 1 || blocks < 1) {
+    cus = 256;
+    blocks = 4;
+  }
+  int w = cus * blocks * kWavesPerBlock;
+  if (w > MOE_PLAN_PARTS) w = MOE_PLAN_PARTS;
+  while (w > kWavesPerBlock && (MOE_PLAN_PARTS % w != 0 || w % kWavesPerBlock != 0)) --w;
+  cache[{dev, kernel}] = w;
+  return w;
+}
+
+}  // namespace moe
 
 namespace {
 

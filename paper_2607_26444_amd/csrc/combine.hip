@@ -2,18 +2,18 @@
 //
 // Token-centric gather-reduce with the same byte-balanced partition as
 // dispatch (one wavefront per part of the plan).  Slot metadata for a batch
-// of 64/k tokens is resolved once, one slot per lane; for each token the
-// wavefront then takes its k source rows and weights from those lanes
-// (readlane into scalar registers) and walks
-// the output row in 1 KiB segments: every lane issues the k independent
-// 16-byte gathers of its segment before it accumulates, keeping k loads per
-// lane in flight, multiplies-adds in float32 and stores 8 bf16 values.  Each
+// of 64/k tokens is resolved once, one slot per lane, and parked in LDS; for
+// each token the wavefront reads its k source rows and weights back at
+// uniform LDS addresses (waiting only on the LDS counter, never on pending
+// stores) and walks the output row in 1 KiB segments: every lane issues the
+// k independent 16-byte gathers of the next segment before it reduces the
+// current one, multiplies-adds in float32 and stores 8 bf16 values.  Each
 // output row has exactly one writer, so the reduction needs no atomics
 // (Section 6.1 accumulates on chip and writes back once).
 //
 // Unused and capacity-dropped slots are redirected to a routed row of the
-// same token and masked out of the sum with a select (not a multiply by 0,
-// which would turn an Inf in that row into NaN).
+// same token, their data is zeroed bitwise and their weight is 0 (a plain
+// multiply by 0 would turn an Inf in that row into NaN).
 
 #include "moe_internal.h"
 
@@ -31,26 +31,97 @@ __device__ __forceinline__ void fma8(float (&acc)[8], const u32x4& v, float w) {
   acc[7] = __builtin_fmaf(w, bf16_hi(v.w), acc[7]);
 }
 
+template <int KW>
+__device__ __forceinline__ void gather(u32x4 (&v)[KW], const uint8_t* const (&src)[KW],
+                                       uint32_t off) {
+#pragma unroll
+  for (int j = 0; j < KW; ++j) v[j] = ld16_stream(src[j] + off);
+}
+
+// Weighted sum of one 1 KiB segment.  MASKED: unused slots read a routed
+// row of the same token; their data is zeroed (bitwise, so an Inf or NaN
+// there cannot leak) and their weight is 0.
+template <int KW, bool MASKED>
+__device__ __forceinline__ u32x4 reduce(const u32x4 (&v)[KW], const float (&wt)[KW],
+                                        const uint32_t (&keep)[KW]) {
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < KW; ++j) {
+    u32x4 x = v[j];
+    if (MASKED) {
+      x.x &= keep[j];
+      x.y &= keep[j];
+      x.z &= keep[j];
+      x.w &= keep[j];
+    }
+    fma8(acc, x, wt[j]);
+  }
+  u32x4 o;
+  o.x = pack_bf16x2(acc[0], acc[1]);
+  o.y = pack_bf16x2(acc[2], acc[3]);
+  o.z = pack_bf16x2(acc[4], acc[5]);
+  o.w = pack_bf16x2(acc[6], acc[7]);
+  return o;
+}
+
+// One token's output row: full 1 KiB segments two at a time, then the
+// ragged tail.  The gathers of the next segment are issued before the
+// current one is reduced and stored, so waiting for them never waits for a
+// store (vector memory operations complete in issue order on this counter).
+template <int KW, bool MASKED>
+__device__ __forceinline__ void combine_row(uint8_t* dst, const uint8_t* const (&src)[KW],
+                                            const float (&wt)[KW],
+                                            const uint32_t (&keep)[KW], uint32_t rb,
+                                            uint32_t l16) {
+  const uint32_t nf = rb / kWaveBytes, tail = rb % kWaveBytes;
+  u32x4 a[KW], b[KW];
+  uint32_t o = l16;
+  if (nf > 0) gather<KW>(a, src, o);
+  for (uint32_t s = 0; s + 2 <= nf; s += 2) {
+    gather<KW>(b, src, o + kWaveBytes);
+    st16(dst + o, reduce<KW, MASKED>(a, wt, keep));
+    if (s + 2 < nf) gather<KW>(a, src, o + 2 * kWaveBytes);
+    st16(dst + o + kWaveBytes, reduce<KW, MASKED>(b, wt, keep));
+    o += 2 * kWaveBytes;
+  }
+  if (nf & 1u) {
+    st16(dst + o, reduce<KW, MASKED>(a, wt, keep));
+    o += kWaveBytes;
+  }
+  if (l16 < tail) {
+    gather<KW>(a, src, o);
+    st16(dst + o, reduce<KW, MASKED>(a, wt, keep));
+  }
+}
+
 // KW: slots resolved per token (>= k).
 template <int KW>
 __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
+  // Per-slot source row and weight of the current batch, one entry per lane
+  // of each wavefront (0 = slot not combined), padded with zeros so a token
+  // can read KW entries without a bounds test.
+  __shared__ uint64_t s_src[kWavesPerBlock][kWave + MOE_MAX_K];
+  __shared__ float s_w[kWavesPerBlock][kWave + MOE_MAX_K];
   const int lane = threadIdx.x & (kWave - 1);
-  const int part = uniform(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
-  if (part >= MOE_PLAN_PARTS) return;
-  const int t0 = a.bound[part], t1 = a.bound[part + 1];
-  const int64_t rb = a.row_bytes;
+  const int wv = threadIdx.x / kWave;
+  const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
+  const int t0 = a.bound[g * a.parts_per_wave], t1 = a.bound[(g + 1) * a.parts_per_wave];
+  const uint32_t rb = (uint32_t)a.row_bytes;
+  const uint32_t l16 = lane * kVecBytes;
   const int k = a.k;
   const int tpb = kWave / k;        // tokens whose slots fit one lane each
   const int lt = lane / k;          // this lane's token within a batch
   const int lj = lane - lt * k;     // ... and its slot
   uint32_t st = 0;
+  if (lane < MOE_MAX_K) {
+    s_src[wv][kWave + lane] = 0;
+    s_w[wv][kWave + lane] = 0.0f;
+  }
 
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
-    // Source row and weight of slot (tb + lt, lj), resolved once per batch.
     uint64_t srow = 0;
     float wl = 0.0f;
-    bool ok = false;
     if (tb + lt < te) {
       const int64_t s = (int64_t)(tb + lt) * k + lj;
       const int p = a.pos[s];
@@ -60,59 +131,46 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
         if (local >= 0 && local < a.recv_cap[r]) {
           srow = a.expert_y[r] + (uint64_t)local * (uint64_t)rb;
           wl = a.topk_w[s];
-          ok = true;
         } else {
           st |= MOE_STATUS_CAPACITY;
         }
       }
     }
-    const uint64_t okm = __ballot(ok);
+    __builtin_amdgcn_wave_barrier();
+    s_src[wv][lane] = srow;
+    s_w[wv][lane] = wl;
+    __builtin_amdgcn_wave_barrier();
 
     for (int t = tb; t < te; ++t) {
       const int l0 = (t - tb) * k;
       const uint8_t* src[KW];
       float wt[KW];
-      bool use[KW];
-      const uint8_t* any = nullptr;
+      uint32_t keep[KW];
+      uint64_t first = 0;
+      bool all = true;
 #pragma unroll
-      for (int j = 0; j < KW; ++j) {
-        src[j] = nullptr;
-        wt[j] = 0.0f;
-        use[j] = j < k && ((okm >> (l0 + j)) & 1ull);
-        if (use[j]) {
-          src[j] = reinterpret_cast<const uint8_t*>(readlane64(srow, l0 + j));
-          wt[j] = readlane_f32(wl, l0 + j);
-          if (!any) any = src[j];
-        }
+      for (int j = KW - 1; j >= 0; --j) {
+        uint64_t sp = readlane64(s_src[wv][l0 + j], 0);
+        const float w = readlane_f32(s_w[wv][l0 + j], 0);
+        sp = (j < k) ? sp : 0;
+        src[j] = reinterpret_cast<const uint8_t*>(sp);
+        wt[j] = sp ? w : 0.0f;
+        keep[j] = sp ? 0xFFFFFFFFu : 0u;
+        all = all && sp;
+        first = sp ? sp : first;
       }
       uint8_t* dst = reinterpret_cast<uint8_t*>(a.y) + (int64_t)t * rb;
-      if (!any) {  // no routed slot: y = +0
-        for (int64_t off = lane * kVecBytes; off < rb; off += kWaveBytes)
-          st16(dst + off, u32x4{0u, 0u, 0u, 0u});
+      if (!first) {  // no routed slot: y = +0
+        for (uint32_t off = l16; off < rb; off += kWaveBytes) st16(dst + off, u32x4{0u, 0u, 0u, 0u});
         continue;
       }
+      if (all) {
+        combine_row<KW, false>(dst, src, wt, keep, rb, l16);
+      } else {
 #pragma unroll
-      for (int j = 0; j < KW; ++j)
-        if (!use[j]) src[j] = any;
-
-#pragma unroll 2
-      for (int64_t seg = 0; seg < rb; seg += kWaveBytes) {
-        const int64_t off = seg + lane * kVecBytes;
-        if (off < rb) {
-          u32x4 v[KW];
-#pragma unroll
-          for (int j = 0; j < KW; ++j) v[j] = ld16(src[j] + off);
-          float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int j = 0; j < KW; ++j)
-            if (use[j]) fma8(acc, v[j], wt[j]);
-          u32x4 o;
-          o.x = pack_bf16x2(acc[0], acc[1]);
-          o.y = pack_bf16x2(acc[2], acc[3]);
-          o.z = pack_bf16x2(acc[4], acc[5]);
-          o.w = pack_bf16x2(acc[6], acc[7]);
-          st16(dst + off, o);
-        }
+        for (int j = 0; j < KW; ++j)
+          if (!keep[j]) src[j] = reinterpret_cast<const uint8_t*>(first);
+        combine_row<KW, true>(dst, src, wt, keep, rb, l16);
       }
     }
   }
@@ -121,9 +179,12 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
 }
 
 template <int KW>
-hipError_t launch_kw(const CombineArgs& a, hipStream_t stream) {
-  const dim3 grid(MOE_PLAN_PARTS / kWavesPerBlock), block(kBlock);
-  hipLaunchKernelGGL((combine_kernel<KW>), grid, block, 0, stream, a);
+hipError_t launch_kw(CombineArgs a, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&combine_kernel<KW>);
+  const int waves = resident_waves(fn, 0);
+  a.parts_per_wave = MOE_PLAN_PARTS / waves;
+  hipLaunchKernelGGL((combine_kernel<KW>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
+                     stream, a);
   return hipGetLastError();
 }
 

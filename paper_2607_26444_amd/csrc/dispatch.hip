@@ -2,10 +2,11 @@
 //
 // Work split (Section 6.2 with one memory tier, Appendix D third level):
 // moe_layout leaves MOE_PLAN_PARTS contiguous token ranges of equal byte
-// cost (a token costs one row read plus one row write per routed slot).  One
-// wavefront takes one part, so every wavefront moves the same number of
-// bytes no matter how skewed the routing is; a hot expert only changes where
-// rows land, not who copies them.
+// cost (a token costs one row read plus one row write per routed slot).  The
+// kernel launches as many wavefronts as the GPU keeps resident and gives
+// each the same number of consecutive parts, so every wavefront moves the
+// same number of bytes no matter how skewed the routing is; a hot expert only
+// changes where rows land, not who copies them.
 //
 // Push direction: a wavefront reads its token's row from x once into
 // registers (16 bytes per lane per 1 KiB segment, so a 14 KiB row is 14
@@ -13,9 +14,10 @@
 // destinations.  x is read exactly once; every destination row is written
 // by exactly one wavefront with full 1 KiB coalesced stores.  Slot metadata
 // (pos, expert, region base, capacity) for a batch of 64/k tokens is loaded
-// once, one slot per lane, before any row moves; the copy loop then takes
-// each destination from its lane with readlane, so no load of metadata sits
-// between row stores.
+// once, one slot per lane, and parked in LDS; the copy loop reads each
+// destination back at a uniform LDS address, so no global load of metadata
+// (whose wait would also wait for every pending row store) sits between
+// row stores.
 
 #include "moe_internal.h"
 
@@ -26,23 +28,31 @@ namespace {
 // FULL: row bytes == VPL KiB exactly (no per-lane tail test).
 template <int VPL, bool FULL, bool SCALES>
 __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
+  // Destination row (and scale row) of every slot of the current batch, one
+  // entry per lane of each wavefront (0 = slot not dispatched), padded with
+  // zeros so a token can read k entries without a bounds test.
+  __shared__ uint64_t s_dst[kWavesPerBlock][kWave + MOE_MAX_K];
+  __shared__ uint64_t s_sdst[kWavesPerBlock][SCALES ? kWave + MOE_MAX_K : 1];
   const int lane = threadIdx.x & (kWave - 1);
-  const int part = uniform(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
-  if (part >= MOE_PLAN_PARTS) return;
-  const int t0 = a.bound[part], t1 = a.bound[part + 1];
-  const int64_t rb = a.row_bytes;
-  const int sb = a.scale_row_bytes;
+  const int wv = threadIdx.x / kWave;
+  const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
+  const int t0 = a.bound[g * a.parts_per_wave], t1 = a.bound[(g + 1) * a.parts_per_wave];
+  const uint32_t rb = (uint32_t)a.row_bytes;
+  const uint32_t sb = (uint32_t)a.scale_row_bytes;
+  const uint32_t l16 = lane * kVecBytes;
   const int k = a.k;
   const int tpb = kWave / k;        // tokens whose slots fit one lane each
   const int lt = lane / k;          // this lane's token within a batch
   const int lj = lane - lt * k;     // ... and its slot
   uint32_t st = 0;
+  if (lane < MOE_MAX_K) {
+    s_dst[wv][kWave + lane] = 0;
+    if (SCALES) s_sdst[wv][kWave + lane] = 0;
+  }
 
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
-    // Destination of slot (tb + lt, lj), resolved once per batch by its lane.
     uint64_t dst = 0, sdst = 0;
-    bool ok = false;
     if (tb + lt < te) {
       const int64_t s = (int64_t)(tb + lt) * k + lj;
       const int p = a.pos[s];
@@ -50,32 +60,34 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
         const int r = a.topk_idx[s] / a.L;
         const int local = p - a.rank_offset[r];
         if (local >= 0 && local < a.recv_cap[r]) {
-          dst = a.recv_x[r] + (uint64_t)local * (uint64_t)rb;
-          if (SCALES) sdst = a.recv_scales[r] + (uint64_t)local * (uint64_t)sb;
-          ok = true;
+          dst = a.recv_x[r] + (uint64_t)local * rb;
+          if (SCALES) sdst = a.recv_scales[r] + (uint64_t)local * sb;
         } else {
           st |= MOE_STATUS_CAPACITY;
         }
       }
     }
-    const uint64_t okm = __ballot(ok);
+    __builtin_amdgcn_wave_barrier();
+    s_dst[wv][lane] = dst;
+    if (SCALES) s_sdst[wv][lane] = sdst;
+    __builtin_amdgcn_wave_barrier();
 
     for (int t = tb; t < te; ++t) {
       const int l0 = (t - tb) * k;
       const uint8_t* src = a.x + (int64_t)t * rb;
-      for (int64_t seg = 0; seg < rb; seg += VPL * kWaveBytes) {
+      for (uint32_t seg = 0; seg < rb; seg += VPL * kWaveBytes) {
         u32x4 v[VPL];
 #pragma unroll
         for (int c = 0; c < VPL; ++c) {
-          const int64_t off = seg + c * kWaveBytes + lane * kVecBytes;
+          const uint32_t off = seg + c * kWaveBytes + l16;
           if (FULL || off < rb) v[c] = ld16(src + off);
         }
         for (int j = 0; j < k; ++j) {
-          if (!((okm >> (l0 + j)) & 1ull)) continue;
-          uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(dst, l0 + j));
+          uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(s_dst[wv][l0 + j], 0));
+          if (!d) continue;
 #pragma unroll
           for (int c = 0; c < VPL; ++c) {
-            const int64_t off = seg + c * kWaveBytes + lane * kVecBytes;
+            const uint32_t off = seg + c * kWaveBytes + l16;
             if (FULL || off < rb) st16(d + off, v[c]);
           }
         }
@@ -83,14 +95,13 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
       if (SCALES) {
         // Block scales, one float32 per lane per pass.
         const uint8_t* ssrc = a.x_scales + (int64_t)t * sb;
-        for (int o = 0; o < sb; o += kWave * 4) {
-          const int off = o + lane * 4;
+        for (uint32_t o = 0; o < sb; o += kWave * 4) {
+          const uint32_t off = o + lane * 4;
           uint32_t sv = 0;
           if (off < sb) sv = ld4(ssrc + off);
           for (int j = 0; j < k; ++j) {
-            if (!((okm >> (l0 + j)) & 1ull)) continue;
-            uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(sdst, l0 + j));
-            if (off < sb) st4(d + off, sv);
+            uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l0 + j], 0));
+            if (d && off < sb) st4(d + off, sv);
           }
         }
       }
@@ -101,9 +112,14 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
 }
 
 template <int VPL, bool SCALES>
-hipError_t launch_vpl(const DispatchArgs& a, hipStream_t stream) {
-  const dim3 grid(MOE_PLAN_PARTS / kWavesPerBlock), block(kBlock);
-  if (a.row_bytes == (int64_t)VPL * kWaveBytes)
+hipError_t launch_vpl(DispatchArgs a, hipStream_t stream) {
+  const bool full = a.row_bytes == (int64_t)VPL * kWaveBytes;
+  const void* fn = full ? reinterpret_cast<const void*>(&dispatch_kernel<VPL, true, SCALES>)
+                        : reinterpret_cast<const void*>(&dispatch_kernel<VPL, false, SCALES>);
+  const int waves = resident_waves(fn, 0);
+  a.parts_per_wave = MOE_PLAN_PARTS / waves;
+  const dim3 grid(waves / kWavesPerBlock), block(kBlock);
+  if (full)
     hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES>), grid, block, 0, stream, a);
   else
     hipLaunchKernelGGL((dispatch_kernel<VPL, false, SCALES>), grid, block, 0, stream, a);

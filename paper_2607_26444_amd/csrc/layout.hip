@@ -11,9 +11,10 @@
 //                 not serialize on a hot expert the way counter atomics do,
 //                 and the result does not depend on arrival order.
 //
-//   layout_place  every chunk reads the whole [nc][E] count matrix (small by
-//                 construction), derives the global per-expert totals, their
-//                 exclusive scan (expert_offset) and its own column prefix,
+//   layout_place  every chunk reads the whole count matrix (small by
+//                 construction, stored expert-major), derives the global
+//                 per-expert totals, their exclusive scan (expert_offset) and
+//                 its own column prefix,
 //                 then rebuilds its bitmaps and gives each routed slot
 //                     pos = expert_offset[e] + (rows of e in earlier chunks)
 //                         + (rows of e in earlier sub-chunks of this chunk)
@@ -85,7 +86,7 @@ __device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* scra
 
 template <int KW>
 __global__ __launch_bounds__(kBlock) void layout_count_kernel(
-    const int32_t* __restrict__ idx, int64_t T, int k, int E, int64_t chunk_tokens,
+    const int32_t* __restrict__ idx, int64_t T, int k, int E, int64_t chunk_tokens, int ncp,
     int32_t* __restrict__ counts, uint32_t* __restrict__ status) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* mask = reinterpret_cast<uint64_t*>(smem);           // [4][E]
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(kBlock) void layout_count_kernel(
     }
     __syncthreads();
   }
-  for (int e = tid; e < E; e += kBlock) counts[(int64_t)blockIdx.x * E + e] = cnt[e];
+  for (int e = tid; e < E; e += kBlock) counts[(int64_t)e * ncp + blockIdx.x] = cnt[e];
   st = wave_or(st);
   if (lane == 0 && st) atomicOr(status, st);
 }
@@ -128,7 +129,7 @@ constexpr int kMaxExpertsPerThread = MOE_MAX_EXPERTS / kBlock;  // 4
 template <int KW>
 __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     const int32_t* __restrict__ idx, int64_t T, int k, int E, int R, int64_t chunk_tokens,
-    int nc, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
+    int nc, int ncp, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
     int32_t* __restrict__ expert_offset, int32_t* __restrict__ rank_count,
     int32_t* __restrict__ rank_offset, int32_t* __restrict__ pos,
     int32_t* __restrict__ row_src, int32_t* __restrict__ bound) {
@@ -150,18 +151,24 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   // e = tid*EPT .. tid*EPT+EPT-1 (contiguous, so a scan over threads is a
   // scan over experts).
   const int ept = (E + kBlock - 1) / kBlock;
+  // The count matrix is expert-major ([E][ncp], ncp = nc rounded up to 4), so
+  // an expert's column is contiguous and arrives in independent 16-byte
+  // loads that are all in flight together.
   int tot[kMaxExpertsPerThread], pre[kMaxExpertsPerThread];
 #pragma unroll
-  for (int q = 0; q < kMaxExpertsPerThread; ++q) tot[q] = pre[q] = 0;
-  for (int cc = 0; cc < nc; ++cc) {
-    const int32_t* row = counts + (int64_t)cc * E;
-#pragma unroll
-    for (int q = 0; q < kMaxExpertsPerThread; ++q) {
-      const int e = tid * ept + q;
-      if (q < ept && e < E) {
-        const int v = row[e];
-        tot[q] += v;
-        pre[q] += (cc < c) ? v : 0;
+  for (int q = 0; q < kMaxExpertsPerThread; ++q) {
+    tot[q] = pre[q] = 0;
+    const int e = tid * ept + q;
+    if (q < ept && e < E) {
+      const int4* col = reinterpret_cast<const int4*>(counts + (int64_t)e * ncp);
+#pragma unroll 8
+      for (int i = 0; i < ncp / 4; ++i) {
+        const int4 v = col[i];
+        const int cc = 4 * i;
+        tot[q] += (cc < nc ? v.x : 0) + (cc + 1 < nc ? v.y : 0) + (cc + 2 < nc ? v.z : 0) +
+                  (cc + 3 < nc ? v.w : 0);
+        pre[q] += (cc < c ? v.x : 0) + (cc + 1 < c ? v.y : 0) + (cc + 2 < c ? v.z : 0) +
+                  (cc + 3 < c ? v.w : 0);
       }
     }
   }
@@ -279,11 +286,11 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
   const size_t lds_place = (size_t)kWavesPerBlock * E * 8 + kWavesPerBlock * 8 +
                            (size_t)E * 4 + (size_t)(E + 1) * 4;
   hipLaunchKernelGGL(layout_count_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_count, stream,
-                     idx, T, k, E, g.chunk_tokens, counts, status);
+                     idx, T, k, E, g.chunk_tokens, g.ncp, counts, status);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(layout_place_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_place, stream,
-                     idx, T, k, E, R, g.chunk_tokens, g.nc, counts, expert_count,
+                     idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
                      expert_offset, rank_count, rank_offset, pos, row_src, bound);
   return hipGetLastError();
 }
@@ -298,8 +305,9 @@ LayoutGeom layout_geom(int64_t T, int E) {
   g.chunk_tokens = kBlock * (per < 1 ? 1 : per);
   g.nc = (int)((T + g.chunk_tokens - 1) / g.chunk_tokens);
   if (g.nc < 1) g.nc = 1;
+  g.ncp = (g.nc + 3) / 4 * 4;
   g.plan_bytes = ((size_t)(MOE_PLAN_PARTS + 1) * 4 + 255) / 256 * 256;
-  g.counts_bytes = (size_t)g.nc * E * 4;
+  g.counts_bytes = (size_t)g.ncp * E * 4;
   g.total = g.plan_bytes + (g.counts_bytes + 255) / 256 * 256;
   return g;
 }

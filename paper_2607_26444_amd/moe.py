@@ -32,7 +32,7 @@ MOE_STATUS_CAPACITY = 4
 MOE_MAX_K = 32
 MOE_MAX_EXPERTS = 1024
 MOE_FP8_BLOCK = 128
-MOE_PLAN_PARTS = 4096
+MOE_PLAN_PARTS = 12288
 
 # Entry points declared in include/moe.h.
 EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error",

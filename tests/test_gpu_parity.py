@@ -52,7 +52,8 @@ def _full_parity(cfg, inp=None, idx=None, w=None, spare_rows=2, cap_delta=None,
     # stand-in expert: bit-exact
     written = np.minimum(ref["layout"]["rank_count"], run.caps)
     h.check_regions(run, run.eregions,
-                    [e.view(np.uint8).reshape(e.shape[0], -1) for e in ref["ey"]], written)
+                    [e.view(np.uint8).reshape(e.shape[0], 2 * e.shape[1]) for e in ref["ey"]],
+                    written)
     # combine: tolerance
     ok, msg = h.combine_close(run.y, ref["y"])
     assert ok, msg
@@ -210,5 +211,8 @@ def test_full_size_workloads(name):
                         combine_on_dispatch=True)
         xf = (inp["x"].astype(np.uint32) << 16).view(np.float32) * np.float32(k)
         want = h.f32_bits_to_bf16_rne(xf)
-        assert np.array_equal(run1.y, want)
+        # the sum starts from +0, so a token whose x is -0 gets +0
+        want[want == 0x8000] = 0
+        bad = run1.y != want
+        assert not bad.any(), (int(bad.sum()), run1.y[bad][:8], want[bad][:8])
         h.log(f"[full] {cfg['name']} unit-weight combine == bf16(k*x) exactly")
