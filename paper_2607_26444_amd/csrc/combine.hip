@@ -9,7 +9,10 @@
 // k independent 16-byte gathers of the next segment before it reduces the
 // current one, multiplies-adds in float32 and stores 8 bf16 values.  Each
 // output row has exactly one writer, so the reduction needs no atomics
-// (Section 6.1 accumulates on chip and writes back once).
+// (Section 6.1 accumulates on chip and writes back once).  Gathers and the
+// output stores are non-temporal: every byte is touched once, and on MI355X
+// keeping them out of the caches measured fastest for the whole
+// dispatch + combine step.
 //
 // Unused and capacity-dropped slots are redirected to a routed row of the
 // same token, their data is zeroed bitwise and their weight is 0 (a plain
@@ -79,18 +82,18 @@ __device__ __forceinline__ void combine_row(uint8_t* dst, const uint8_t* const (
   if (nf > 0) gather<KW>(a, src, o);
   for (uint32_t s = 0; s + 2 <= nf; s += 2) {
     gather<KW>(b, src, o + kWaveBytes);
-    st16(dst + o, reduce<KW, MASKED>(a, wt, keep));
+    st16_stream(dst + o, reduce<KW, MASKED>(a, wt, keep));
     if (s + 2 < nf) gather<KW>(a, src, o + 2 * kWaveBytes);
-    st16(dst + o + kWaveBytes, reduce<KW, MASKED>(b, wt, keep));
+    st16_stream(dst + o + kWaveBytes, reduce<KW, MASKED>(b, wt, keep));
     o += 2 * kWaveBytes;
   }
   if (nf & 1u) {
-    st16(dst + o, reduce<KW, MASKED>(a, wt, keep));
+    st16_stream(dst + o, reduce<KW, MASKED>(a, wt, keep));
     o += kWaveBytes;
   }
   if (l16 < tail) {
     gather<KW>(a, src, o);
-    st16(dst + o, reduce<KW, MASKED>(a, wt, keep));
+    st16_stream(dst + o, reduce<KW, MASKED>(a, wt, keep));
   }
 }
 
@@ -161,7 +164,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
       }
       uint8_t* dst = reinterpret_cast<uint8_t*>(a.y) + (int64_t)t * rb;
       if (!first) {  // no routed slot: y = +0
-        for (uint32_t off = l16; off < rb; off += kWaveBytes) st16(dst + off, u32x4{0u, 0u, 0u, 0u});
+        for (uint32_t off = l16; off < rb; off += kWaveBytes) st16_stream(dst + off, u32x4{0u, 0u, 0u, 0u});
         continue;
       }
       if (all) {
