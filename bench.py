@@ -153,15 +153,16 @@ def main(argv=None):
     counts = lay.rank_count.cpu().numpy()
     rows = [max(1, int(c)) for c in counts]
     rb, sb = wl.row_bytes(cfg), wl.scale_row_bytes(cfg)
+    spitch = (sb + 127) // 128 * 128   # scale rows on whole 128-byte lines
     regions = moe.Regions(rows, rb)
-    sregions = moe.Regions(rows, sb) if fp8 else None
+    sregions = moe.Regions(rows, spitch) if fp8 else None
     eregions = moe.Regions(rows, 2 * H)
     y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
 
     def dispatch():
         moe.moe_dispatch(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
                          regions.table, sregions.table if fp8 else None, regions.cap,
-                         lay.workspace, lay.status)
+                         lay.workspace, lay.status, scale_pitch=spitch)
 
     def combine():
         moe.moe_combine(eregions.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset,
@@ -171,7 +172,7 @@ def main(argv=None):
     dispatch()
     moe.moe_expert_scale(regions.table, sregions.table if fp8 else None, dtype, H, E, R,
                          cfg["expert"] == "identity", lay.expert_offset, lay.rank_offset,
-                         regions.cap, eregions.table, T * k)
+                         regions.cap, eregions.table, T * k, scale_pitch=spitch)
     torch.cuda.synchronize()
 
     for _ in range(a.warmup):

@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define MOE_VERSION 1
+#define MOE_VERSION 2
 
 #define MOE_OK 0
 #define MOE_EINVAL (-1)
@@ -147,7 +147,15 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
  * recv_x    [R] uint64 region base addresses (device table), 16-byte aligned;
  *           region r holds recv_cap[r] rows of row_bytes each.
  * recv_scales [R] uint64 scale-region bases (FP8_E4M3) or NULL; region r
- *           holds recv_cap[r] rows of (H/128)*4 bytes, 4-byte aligned.
+ *           holds recv_cap[r] rows spaced scale_pitch bytes apart.
+ * scale_pitch bytes from one scale row to the next in a scale region; 0
+ *           means packed rows of (H/128)*4 bytes.  Otherwise at least
+ *           (H/128)*4 and a multiple of 4.  Dispatch writes the whole pitch:
+ *           the row's scales, then zeros.  A pitch that is a multiple of 128
+ *           (with 128-byte aligned region bases) gives every scale row its
+ *           own cache lines, so no two rows share a line that different
+ *           wavefronts write partially; packed 224-byte rows cost ~30 us more
+ *           per 131k rows on MI355X.
  * recv_cap  [R] int32 capacity of each region in rows.
  * topk_idx, pos, rank_offset, workspace: as produced by moe_layout.
  * Bytes of a region beyond the rows dispatch writes are left untouched.
@@ -155,7 +163,7 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
 int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H,
                  int k, int E, int R, const int32_t* topk_idx, const int32_t* pos,
                  const int32_t* rank_offset, const uint64_t* recv_x,
-                 const uint64_t* recv_scales, const int32_t* recv_cap,
+                 const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
                  const void* workspace, size_t workspace_bytes, uint32_t* status,
                  void* stream);
 
@@ -189,12 +197,14 @@ int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H,
  * step a separately rounded float32 operation (no fused multiply-add) and
  * the result rounded to bf16 to nearest-even.
  *
- * recv_x / recv_scales: region tables as for moe_dispatch (dtype selects the
- * payload); out_y: [R] uint64 bf16 output regions (rows of 2H bytes).
+ * recv_x / recv_scales / scale_pitch: region tables as for moe_dispatch
+ * (dtype selects the payload); out_y: [R] uint64 bf16 output regions (rows of
+ * 2H bytes).
  * max_rows: an upper bound on expert_offset[E] (normally T*k).
  */
-int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int dtype, int H,
-                     int E, int R, int identity, const int32_t* expert_offset,
+int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int scale_pitch,
+                     int dtype, int H, int E, int R, int identity,
+                     const int32_t* expert_offset,
                      const int32_t* rank_offset, const int32_t* recv_cap,
                      const uint64_t* out_y, int64_t max_rows, void* stream);
 

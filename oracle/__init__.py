@@ -44,9 +44,9 @@ def lib():
         L.oracle_fp8e4m3_to_float.restype = ctypes.c_float
         L.oracle_layout.argtypes = [P_, I64, I32, I32, I32, P_, P_, P_, P_, P_, P_, P_]
         L.oracle_plan.argtypes = [P_, I64, I32, I32, P_]
-        L.oracle_dispatch.argtypes = [P_, I64, P_, I64, I64, I32, I32, I32, P_, P_,
+        L.oracle_dispatch.argtypes = [P_, I64, P_, I64, I64, I64, I32, I32, I32, P_, P_,
                                       P_, P_, P_, P_, P_]
-        L.oracle_expert_scale.argtypes = [P_, P_, I32, I32, I32, I32, I32, P_, P_,
+        L.oracle_expert_scale.argtypes = [P_, P_, I64, I32, I32, I32, I32, I32, P_, P_,
                                           P_, P_]
         L.oracle_combine.argtypes = [P_, P_, I64, I32, I32, I32, I32, P_, P_, P_,
                                      P_, P_, P_]
@@ -115,12 +115,13 @@ def plan(pos: np.ndarray, T: int, k: int, P: int) -> np.ndarray:
 
 # ---------------------------------------------------------------- dispatch
 def dispatch(x_rows: np.ndarray, x_scale_rows, topk_idx, pos, rank_offset,
-             E: int, R: int, recv_cap, sentinel: int = 0xA5):
+             E: int, R: int, recv_cap, sentinel: int = 0xA5, scale_pitch: int = 0):
     """Copy routed rows into R regions.
 
     x_rows: uint8 [T, row_bytes]; x_scale_rows: uint8 [T, scale_row_bytes] or
     None.  Regions are uint8 [recv_cap[r], row_bytes] pre-filled with
-    `sentinel`.  Returns (regions, scale_regions or None, status).
+    `sentinel`; scale regions uint8 [recv_cap[r], scale_pitch] (0: packed).
+    Returns (regions, scale_regions or None, status).
     """
     x_rows = np.ascontiguousarray(x_rows, dtype=np.uint8)
     T, rb = x_rows.shape
@@ -131,13 +132,15 @@ def dispatch(x_rows: np.ndarray, x_scale_rows, topk_idx, pos, rank_offset,
     if x_scale_rows is not None:
         xs = np.ascontiguousarray(x_scale_rows, dtype=np.uint8)
         srb = xs.shape[1]
-        sregs = [np.full((int(c), srb), sentinel, np.uint8) for c in cap]
+        scale_pitch = scale_pitch or srb
+        assert scale_pitch >= srb
+        sregs = [np.full((int(c), scale_pitch), sentinel, np.uint8) for c in cap]
     st = np.zeros(1, np.uint32)
     idx = np.ascontiguousarray(topk_idx, dtype=np.int32)
     pos = np.ascontiguousarray(pos, dtype=np.int32)
     ro = np.ascontiguousarray(rank_offset, dtype=np.int32)
     rc = lib().oracle_dispatch(_p(x_rows), rb, _p(xs) if xs is not None else None,
-                               srb, T, k, E, R, _p(idx), _p(pos), _p(ro),
+                               srb, scale_pitch, T, k, E, R, _p(idx), _p(pos), _p(ro),
                                _ptr_table(regs),
                                _ptr_table(sregs) if sregs is not None else None,
                                _p(cap), _p(st))
@@ -148,14 +151,16 @@ def dispatch(x_rows: np.ndarray, x_scale_rows, topk_idx, pos, rank_offset,
 # ---------------------------------------------------------------- expert
 def expert_scale(regions, scale_regions, payload_fp8: bool, H: int, E: int,
                  R: int, identity: bool, expert_offset, rank_offset, recv_cap):
-    """Stand-in expert: bf16 regions [recv_cap[r], H] of s_e * row."""
+    """Stand-in expert: bf16 regions [recv_cap[r], H] of s_e * row.  Scale
+    regions are [rows, scale_pitch] arrays (the pitch is their width)."""
     cap = np.ascontiguousarray(recv_cap, dtype=np.int32)
     outs = [np.zeros((int(c), H), np.uint16) for c in cap]
     eo = np.ascontiguousarray(expert_offset, dtype=np.int32)
     ro = np.ascontiguousarray(rank_offset, dtype=np.int32)
+    pitch = scale_regions[0].shape[1] if scale_regions else 0
     rc = lib().oracle_expert_scale(
         _ptr_table(regions),
-        _ptr_table(scale_regions) if scale_regions is not None else None,
+        _ptr_table(scale_regions) if scale_regions is not None else None, pitch,
         int(bool(payload_fp8)), H, E, R, int(bool(identity)), _p(eo), _p(ro),
         _p(cap), _ptr_table(outs))
     _check(rc, "oracle_expert_scale")

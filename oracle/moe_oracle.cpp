@@ -186,11 +186,13 @@ int oracle_plan(const int32_t* pos, int64_t T, int32_t k, int32_t P,
 // Dispatch (Section 6.1 remote-slice transfers, one per routed slot: source
 // row t of x, destination peer r, destination row pos - rank_offset[r] of
 // that peer's receive region).  A pure byte copy of the row and, for fp8
-// payloads, of its row of block scales.  recv_x[r] / recv_s[r] are host
-// pointers to region r; recv_cap[r] is its capacity in rows.
+// payloads, of its row of block scales; scale rows sit scale_pitch bytes
+// apart and the bytes of a pitch past the scales are set to zero.
+// recv_x[r] / recv_s[r] are host pointers to region r; recv_cap[r] is its
+// capacity in rows.
 // ---------------------------------------------------------------------------
 int oracle_dispatch(const uint8_t* x, int64_t row_bytes, const uint8_t* x_scales,
-                    int64_t scale_row_bytes, int64_t T, int32_t k, int32_t E,
+                    int64_t scale_row_bytes, int64_t scale_pitch, int64_t T, int32_t k, int32_t E,
                     int32_t R, const int32_t* topk_idx, const int32_t* pos,
                     const int32_t* rank_offset, uint8_t* const* recv_x,
                     uint8_t* const* recv_s, const int32_t* recv_cap,
@@ -206,9 +208,11 @@ int oracle_dispatch(const uint8_t* x, int64_t row_bytes, const uint8_t* x_scales
       int64_t local = (int64_t)p - rank_offset[r];
       if (local >= recv_cap[r]) { st |= kCapacity; continue; }
       std::memcpy(recv_x[r] + local * row_bytes, x + t * row_bytes, (size_t)row_bytes);
-      if (x_scales)
-        std::memcpy(recv_s[r] + local * scale_row_bytes, x_scales + t * scale_row_bytes,
-                    (size_t)scale_row_bytes);
+      if (x_scales) {
+        uint8_t* srow = recv_s[r] + local * scale_pitch;
+        std::memcpy(srow, x_scales + t * scale_row_bytes, (size_t)scale_row_bytes);
+        for (int64_t b = scale_row_bytes; b < scale_pitch; ++b) srow[b] = 0;
+      }
     }
   }
   *status |= st;
@@ -224,14 +228,13 @@ int oracle_dispatch(const uint8_t* x, int64_t row_bytes, const uint8_t* x_scales
 // even).  Region r holds rows of experts r*L .. r*L+L-1 in expert order;
 // expert_offset / rank_offset come from oracle_layout.
 // ---------------------------------------------------------------------------
-int oracle_expert_scale(uint8_t* const* recv_x, uint8_t* const* recv_s,
+int oracle_expert_scale(uint8_t* const* recv_x, uint8_t* const* recv_s, int64_t scale_pitch,
                         int32_t payload_fp8, int32_t H, int32_t E, int32_t R,
                         int32_t identity, const int32_t* expert_offset,
                         const int32_t* rank_offset, const int32_t* recv_cap,
                         uint16_t* const* out) {
   if (H < 1 || E < 1 || R < 1 || E % R != 0) return -1;
   const int32_t L = E / R;
-  const int32_t nblk = H / 128;
   for (int32_t e = 0; e < E; ++e) {
     const int32_t r = e / L;
     const float se = identity ? 1.0f : 1.0f + 0.01f * (float)e;
@@ -247,7 +250,7 @@ int oracle_expert_scale(uint8_t* const* recv_x, uint8_t* const* recv_s,
         } else {
           const uint8_t* in = recv_x[r] + local * H;
           float sc;
-          std::memcpy(&sc, recv_s[r] + (local * nblk + h / 128) * 4, 4);
+          std::memcpy(&sc, recv_s[r] + local * scale_pitch + (h / 128) * 4, 4);
           float dq = oracle_fp8e4m3_to_float(in[h]) * sc;
           v = dq * se;
         }

@@ -103,9 +103,9 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R, int32_t*
 
 int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k, int E,
                  int R, const int32_t* topk_idx, const int32_t* pos, const int32_t* rank_offset,
-                 const uint64_t* recv_x, const uint64_t* recv_scales, const int32_t* recv_cap,
-                 const void* workspace, size_t workspace_bytes, uint32_t* status,
-                 void* stream) {
+                 const uint64_t* recv_x, const uint64_t* recv_scales, int scale_pitch,
+                 const int32_t* recv_cap, const void* workspace, size_t workspace_bytes,
+                 uint32_t* status, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1 || (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3)) return MOE_EINVAL;
@@ -116,6 +116,10 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
   const int64_t row_bytes = fp8 ? (int64_t)H : 2 * (int64_t)H;
   if (row_bytes % 16 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
   if (!aligned(x, 16) || (fp8 && !aligned(x_scales, 4))) return MOE_EALIGN;
+  const int scale_row = fp8 ? (H / MOE_FP8_BLOCK) * 4 : 0;
+  const int pitch = (fp8 && scale_pitch == 0) ? scale_row : scale_pitch;
+  if (fp8 && (pitch < scale_row)) return MOE_EINVAL;
+  if (fp8 && pitch % 4 != 0) return MOE_EALIGN;
   if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
     return MOE_EWORKSPACE;
   if (T == 0) return MOE_OK;
@@ -123,7 +127,8 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
   a.x = static_cast<const uint8_t*>(x);
   a.x_scales = fp8 ? reinterpret_cast<const uint8_t*>(x_scales) : nullptr;
   a.row_bytes = row_bytes;
-  a.scale_row_bytes = fp8 ? (H / MOE_FP8_BLOCK) * 4 : 0;
+  a.scale_row_bytes = scale_row;
+  a.scale_pitch = fp8 ? pitch : 0;
   a.k = k;
   a.L = E / R;
   a.topk_idx = topk_idx;
@@ -166,10 +171,11 @@ int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H,
   return launched(moe::launch_combine(a, as_stream(stream)));
 }
 
-int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int dtype, int H,
-                     int E, int R, int identity, const int32_t* expert_offset,
-                     const int32_t* rank_offset, const int32_t* recv_cap, const uint64_t* out_y,
-                     int64_t max_rows, void* stream) {
+int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int scale_pitch,
+                     int dtype, int H, int E, int R, int identity,
+                     const int32_t* expert_offset, const int32_t* rank_offset,
+                     const int32_t* recv_cap, const uint64_t* out_y, int64_t max_rows,
+                     void* stream) {
   if (H < 1 || E < 1 || E > MOE_MAX_EXPERTS || R < 1 || E % R != 0 || max_rows < 0)
     return MOE_EINVAL;
   if (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3) return MOE_EINVAL;
@@ -177,10 +183,15 @@ int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int dt
   if (!recv_x || !expert_offset || !rank_offset || !recv_cap || !out_y) return MOE_EINVAL;
   if (fp8 && !recv_scales) return MOE_EINVAL;
   if (H % 8 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
+  const int scale_row = fp8 ? (H / MOE_FP8_BLOCK) * 4 : 0;
+  const int pitch = (fp8 && scale_pitch == 0) ? scale_row : scale_pitch;
+  if (fp8 && pitch < scale_row) return MOE_EINVAL;
+  if (fp8 && pitch % 4 != 0) return MOE_EALIGN;
   if (max_rows == 0) return MOE_OK;
   moe::ExpertArgs a;
   a.recv_x = recv_x;
   a.recv_scales = fp8 ? recv_scales : nullptr;
+  a.scale_pitch = fp8 ? pitch : 0;
   a.H = H;
   a.E = E;
   a.L = E / R;

@@ -39,6 +39,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
   const int t0 = a.bound[g * a.parts_per_wave], t1 = a.bound[(g + 1) * a.parts_per_wave];
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t sb = (uint32_t)a.scale_row_bytes;
+  const uint32_t sp = (uint32_t)a.scale_pitch;
   const uint32_t l16 = lane * kVecBytes;
   const int k = a.k;
   const int tpb = kWave / k;        // tokens whose slots fit one lane each
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
         const int local = p - a.rank_offset[r];
         if (local >= 0 && local < a.recv_cap[r]) {
           dst = a.recv_x[r] + (uint64_t)local * rb;
-          if (SCALES) sdst = a.recv_scales[r] + (uint64_t)local * sb;
+          if (SCALES) sdst = a.recv_scales[r] + (uint64_t)local * sp;
         } else {
           st |= MOE_STATUS_CAPACITY;
         }
@@ -75,6 +76,13 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     for (int t = tb; t < te; ++t) {
       const int l0 = (t - tb) * k;
       const uint8_t* src = a.x + (int64_t)t * rb;
+      const uint8_t* ssrc = SCALES ? a.x_scales + (int64_t)t * sb : nullptr;
+      // Scale rows (pitch up to 1 KiB, sizes in 16-byte multiples) move with
+      // the row: lane l carries bytes [16 l, 16 l + 16) of the pitched row,
+      // scales first, zeros after.
+      const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
+      u32x4 sv = {0u, 0u, 0u, 0u};
+      if (s16 && l16 < sb) sv = ld16(ssrc + l16);
       for (uint32_t seg = 0; seg < rb; seg += VPL * kWaveBytes) {
         u32x4 v[VPL];
 #pragma unroll
@@ -90,18 +98,21 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
             const uint32_t off = seg + c * kWaveBytes + l16;
             if (FULL || off < rb) st16(d + off, v[c]);
           }
+          if (s16 && seg == 0) {
+            uint8_t* sd = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l0 + j], 0));
+            if (l16 < sp) st16(sd + l16, sv);
+          }
         }
       }
-      if (SCALES) {
-        // Block scales, one float32 per lane per pass.
-        const uint8_t* ssrc = a.x_scales + (int64_t)t * sb;
-        for (uint32_t o = 0; o < sb; o += kWave * 4) {
+      if (SCALES && !s16) {
+        // Other scale-row sizes: one float32 per lane per pass.
+        for (uint32_t o = 0; o < sp; o += kWave * 4) {
           const uint32_t off = o + lane * 4;
-          uint32_t sv = 0;
-          if (off < sb) sv = ld4(ssrc + off);
+          uint32_t s4 = 0;
+          if (off < sb) s4 = ld4(ssrc + off);
           for (int j = 0; j < k; ++j) {
             uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l0 + j], 0));
-            if (d && off < sb) st4(d + off, sv);
+            if (d && off < sp) st4(d + off, s4);
           }
         }
       }

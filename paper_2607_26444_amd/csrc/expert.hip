@@ -56,7 +56,7 @@ __global__ __launch_bounds__(kBlock) void expert_scale_kernel(ExpertArgs a) {
     } else {
       const uint8_t* in = reinterpret_cast<const uint8_t*>(a.recv_x[r]) + local * (int64_t)a.H;
       const uint8_t* sc = reinterpret_cast<const uint8_t*>(a.recv_scales[r]) +
-                          local * (int64_t)(a.H / MOE_FP8_BLOCK) * 4;
+                          local * (int64_t)a.scale_pitch;
       // 16 fp8 values per lane; 16 divides 128, so they share one block scale.
       for (int64_t off = lane * kVecBytes; off < a.H; off += kWaveBytes) {
         const u32x4 q = ld16(in + off);

@@ -1,7 +1,8 @@
 // Token placement and partition plan (paper Appendix D, first to third
 // level; Section 6.2 for the byte-balanced split).
 //
-// Two kernels, both one workgroup per chunk of tokens:
+// Two kernels, both one workgroup per chunk of tokens (a batch of at most
+// 256 tokens needs only the second, which then counts for itself):
 //
 //   layout_count  per-chunk expert histogram.  Each wavefront owns 64
 //                 consecutive tokens (one per lane) and sets, for every
@@ -126,13 +127,16 @@ __global__ __launch_bounds__(kBlock) void layout_count_kernel(
 
 constexpr int kMaxExpertsPerThread = MOE_MAX_EXPERTS / kBlock;  // 4
 
-template <int KW>
+// SINGLE: the whole batch is one sub-chunk (T <= kBlock), so this kernel
+// also does the counting (no layout_count launch): the totals are the
+// popcounts of its own bitmaps.
+template <int KW, bool SINGLE>
 __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     const int32_t* __restrict__ idx, int64_t T, int k, int E, int R, int64_t chunk_tokens,
     int nc, int ncp, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
     int32_t* __restrict__ expert_offset, int32_t* __restrict__ rank_count,
     int32_t* __restrict__ rank_offset, int32_t* __restrict__ pos,
-    int32_t* __restrict__ row_src, int32_t* __restrict__ bound) {
+    int32_t* __restrict__ row_src, int32_t* __restrict__ bound, uint32_t* __restrict__ status) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* mask = reinterpret_cast<uint64_t*>(smem);               // [4][E]
   int64_t* scan = reinterpret_cast<int64_t*>(mask + kWavesPerBlock * E);  // [4]
@@ -147,28 +151,50 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
 
   for (int i = tid; i < kWavesPerBlock * E; i += kBlock) mask[i] = 0;
 
+  // The first sub-chunk's indices are requested before the count matrix so
+  // both global-memory round trips overlap.
+  int ev0[KW];
+  bool ok0[KW];
+  uint32_t st = 0;
+  load_row<KW>(idx, c0 + tid, c1, k, E, ev0, ok0, st);
+
   // Totals and this chunk's prefix for the experts this thread owns:
   // e = tid*EPT .. tid*EPT+EPT-1 (contiguous, so a scan over threads is a
   // scan over experts).
   const int ept = (E + kBlock - 1) / kBlock;
-  // The count matrix is expert-major ([E][ncp], ncp = nc rounded up to 4), so
-  // an expert's column is contiguous and arrives in independent 16-byte
-  // loads that are all in flight together.
   int tot[kMaxExpertsPerThread], pre[kMaxExpertsPerThread];
+  if (SINGLE) {
+    __syncthreads();
 #pragma unroll
-  for (int q = 0; q < kMaxExpertsPerThread; ++q) {
-    tot[q] = pre[q] = 0;
-    const int e = tid * ept + q;
-    if (q < ept && e < E) {
-      const int4* col = reinterpret_cast<const int4*>(counts + (int64_t)e * ncp);
+    for (int j = 0; j < KW; ++j)
+      if (ok0[j]) atomicOr(&mask[w * E + ev0[j]], 1ull << lane);
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kMaxExpertsPerThread; ++q) {
+      tot[q] = pre[q] = 0;
+      const int e = tid * ept + q;
+      if (q < ept && e < E)
+        for (int ww = 0; ww < kWavesPerBlock; ++ww) tot[q] += __popcll(mask[ww * E + e]);
+    }
+  } else {
+    // The count matrix is expert-major ([E][ncp], ncp = nc rounded up to 4),
+    // so an expert's column is contiguous and arrives in independent 16-byte
+    // loads that are all in flight together.
+#pragma unroll
+    for (int q = 0; q < kMaxExpertsPerThread; ++q) {
+      tot[q] = pre[q] = 0;
+      const int e = tid * ept + q;
+      if (q < ept && e < E) {
+        const int4* col = reinterpret_cast<const int4*>(counts + (int64_t)e * ncp);
 #pragma unroll 8
-      for (int i = 0; i < ncp / 4; ++i) {
-        const int4 v = col[i];
-        const int cc = 4 * i;
-        tot[q] += (cc < nc ? v.x : 0) + (cc + 1 < nc ? v.y : 0) + (cc + 2 < nc ? v.z : 0) +
-                  (cc + 3 < nc ? v.w : 0);
-        pre[q] += (cc < c ? v.x : 0) + (cc + 1 < c ? v.y : 0) + (cc + 2 < c ? v.z : 0) +
-                  (cc + 3 < c ? v.w : 0);
+        for (int i = 0; i < ncp / 4; ++i) {
+          const int4 v = col[i];
+          const int cc = 4 * i;
+          tot[q] += (cc < nc ? v.x : 0) + (cc + 1 < nc ? v.y : 0) + (cc + 2 < nc ? v.z : 0) +
+                    (cc + 3 < nc ? v.w : 0);
+          pre[q] += (cc < c ? v.x : 0) + (cc + 1 < c ? v.y : 0) + (cc + 2 < c ? v.z : 0) +
+                    (cc + 3 < c ? v.w : 0);
+        }
       }
     }
   }
@@ -178,10 +204,13 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     my_tot += tot[q];
     my_pre += pre[q];
   }
-  int64_t n_total = 0;
-  int64_t run = block_exclusive_scan(my_tot, scan, n_total);  // rows before my experts
-  int64_t pre_total = 0;
-  (void)block_exclusive_scan(my_pre, scan, pre_total);         // routed slots before chunk
+  // One scan for both sums: totals in the high 32 bits, this chunk's prefix
+  // in the low 32 (all sums are below 2^31, so no carry crosses).
+  int64_t packed_total = 0;
+  const int64_t packed = block_exclusive_scan((my_tot << 32) | my_pre, scan, packed_total);
+  int64_t run = packed >> 32;                      // rows before my experts
+  const int64_t n_total = packed_total >> 32;       // routed slots N
+  const int64_t pre_total = packed_total & 0xFFFFFFFFll;  // routed slots before chunk
 #pragma unroll
   for (int q = 0; q < kMaxExpertsPerThread; ++q) {
     const int e = tid * ept + q;
@@ -216,20 +245,29 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   const int64_t A = T + n_total;
   int64_t cost_base = c0 + pre_total;
 
-  uint32_t st_unused = 0;
   for (int64_t s0 = c0; s0 < c1; s0 += kBlock) {
     const int64_t t = s0 + tid;
     int ev[KW];
     bool ok[KW];
-    load_row<KW>(idx, t, c1, k, E, ev, ok, st_unused);
+    if (s0 == c0) {
+#pragma unroll
+      for (int j = 0; j < KW; ++j) {
+        ev[j] = ev0[j];
+        ok[j] = ok0[j];
+      }
+    } else {
+      uint32_t st_more = 0;
+      load_row<KW>(idx, t, c1, k, E, ev, ok, st_more);
+    }
     int nvalid = 0;
 #pragma unroll
-    for (int j = 0; j < KW; ++j)
-      if (ok[j]) {
-        atomicOr(&mask[w * E + ev[j]], 1ull << lane);
-        ++nvalid;
-      }
-    __syncthreads();
+    for (int j = 0; j < KW; ++j) nvalid += ok[j] ? 1 : 0;
+    if (!SINGLE) {
+#pragma unroll
+      for (int j = 0; j < KW; ++j)
+        if (ok[j]) atomicOr(&mask[w * E + ev[j]], 1ull << lane);
+      __syncthreads();
+    }
     const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
     for (int j = 0; j < KW; ++j) {
@@ -271,6 +309,10 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   // Rows past the last routed slot have no source.
   for (int64_t i = n_total + (int64_t)c * kBlock + tid; i < T * k; i += (int64_t)nc * kBlock)
     row_src[i] = -1;
+  if (SINGLE) {
+    st = wave_or(st);
+    if (lane == 0 && st) atomicOr(status, st);
+  }
 }
 
 template <int KW>
@@ -285,13 +327,19 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
   const size_t lds_count = (size_t)kWavesPerBlock * E * 8 + (size_t)E * 4;
   const size_t lds_place = (size_t)kWavesPerBlock * E * 8 + kWavesPerBlock * 8 +
                            (size_t)E * 4 + (size_t)(E + 1) * 4;
+  if (g.nc == 1 && T <= kBlock) {
+    hipLaunchKernelGGL((layout_place_kernel<KW, true>), dim3(1), dim3(kBlock), lds_place, stream,
+                       idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
+                       expert_offset, rank_count, rank_offset, pos, row_src, bound, status);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(layout_count_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_count, stream,
                      idx, T, k, E, g.chunk_tokens, g.ncp, counts, status);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(layout_place_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_place, stream,
-                     idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
-                     expert_offset, rank_count, rank_offset, pos, row_src, bound);
+  hipLaunchKernelGGL((layout_place_kernel<KW, false>), dim3(g.nc), dim3(kBlock), lds_place,
+                     stream, idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
+                     expert_offset, rank_count, rank_offset, pos, row_src, bound, status);
   return hipGetLastError();
 }
 

@@ -54,6 +54,7 @@ struct DispatchArgs {
   const uint8_t* x_scales;     // nullptr for bf16 payloads
   int64_t row_bytes;           // 2H (bf16) or H (fp8)
   int32_t scale_row_bytes;     // (H/128)*4 or 0
+  int32_t scale_pitch;         // bytes between scale rows of a region (>= scale_row_bytes)
   int32_t k;
   int32_t L;                   // experts per rank
   const int32_t* topk_idx;
@@ -90,6 +91,7 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 struct ExpertArgs {
   const uint64_t* recv_x;
   const uint64_t* recv_scales;
+  int32_t scale_pitch;
   int32_t H;
   int32_t E;
   int32_t L;

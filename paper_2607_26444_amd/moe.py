@@ -70,10 +70,10 @@ def lib() -> ctypes.CDLL:
         L.moe_last_hip_error.restype = I32
         L.moe_layout_workspace_bytes.argtypes = [I64, I32, I32, I32, ctypes.POINTER(SZ)]
         L.moe_layout.argtypes = [P, I64, I32, I32, I32, P, P, P, P, P, P, P, SZ, P, P]
-        L.moe_dispatch.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, P,
-                                   P, SZ, P, P]
+        L.moe_dispatch.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, I32,
+                                   P, P, SZ, P, P]
         L.moe_combine.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P, P]
-        L.moe_expert_scale.argtypes = [P, P, I32, I32, I32, I32, I32, P, P, P, P, I64, P]
+        L.moe_expert_scale.argtypes = [P, P, I32, I32, I32, I32, I32, I32, P, P, P, P, I64, P]
         for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_dispatch",
                   "moe_combine", "moe_expert_scale"):
             getattr(L, f).restype = I32
@@ -120,11 +120,11 @@ def moe_layout(topk_idx, E, R, expert_count, expert_offset, rank_count, rank_off
 
 
 def moe_dispatch(x, x_scales, dtype, H, E, R, topk_idx, pos, rank_offset, recv_x,
-                 recv_scales, recv_cap, workspace, status, stream=None):
+                 recv_scales, recv_cap, workspace, status, stream=None, scale_pitch=0):
     T, k = topk_idx.shape
     _check("moe_dispatch", lib().moe_dispatch(
         _ptr(x), _ptr(x_scales), dtype, T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
-        _ptr(rank_offset), _ptr(recv_x), _ptr(recv_scales), _ptr(recv_cap),
+        _ptr(rank_offset), _ptr(recv_x), _ptr(recv_scales), scale_pitch, _ptr(recv_cap),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(status),
         _stream(stream)))
 
@@ -139,9 +139,9 @@ def moe_combine(expert_y, topk_w, H, E, R, topk_idx, pos, rank_offset, recv_cap,
 
 
 def moe_expert_scale(recv_x, recv_scales, dtype, H, E, R, identity, expert_offset,
-                     rank_offset, recv_cap, out_y, max_rows, stream=None):
+                     rank_offset, recv_cap, out_y, max_rows, stream=None, scale_pitch=0):
     _check("moe_expert_scale", lib().moe_expert_scale(
-        _ptr(recv_x), _ptr(recv_scales), dtype, H, E, R, int(bool(identity)),
+        _ptr(recv_x), _ptr(recv_scales), scale_pitch, dtype, H, E, R, int(bool(identity)),
         _ptr(expert_offset), _ptr(rank_offset), _ptr(recv_cap), _ptr(out_y), max_rows,
         _stream(stream)))
 

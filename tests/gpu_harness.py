@@ -40,7 +40,7 @@ class GpuRun:
     """One pass of layout -> dispatch -> expert -> combine on the GPU."""
 
     def __init__(self, cfg, inp, topk_idx=None, topk_w=None, spare_rows=0,
-                 cap_delta=None, identity=None, combine_on_dispatch=False):
+                 cap_delta=None, identity=None, combine_on_dispatch=False, scale_pitch=None):
         self.cfg = cfg
         T, H, E, R = cfg["T"], cfg["H"], cfg["E"], cfg["R"]
         idx = inp["topk_idx"] if topk_idx is None else topk_idx
@@ -64,17 +64,20 @@ class GpuRun:
         rows = [int(c) for c in self.caps]
 
         rb, sb = wl.row_bytes(cfg), wl.scale_row_bytes(cfg)
+        # default scale pitch: rows rounded up to whole 128-byte lines
+        self.scale_pitch = (sb + 127) // 128 * 128 if scale_pitch is None else (scale_pitch or sb)
         self.regions = moe.Regions(rows, rb, guard_bytes=GUARD, fill=SENTINEL)
         cap_d = to_dev(self.caps)
         self.sregions = None
         x_d = to_dev(u8_rows(inp["x"]))
         xs_d = None
         if fp8:
-            self.sregions = moe.Regions(rows, sb, guard_bytes=GUARD, fill=SENTINEL)
+            self.sregions = moe.Regions(rows, self.scale_pitch, guard_bytes=GUARD,
+                                        fill=SENTINEL)
             xs_d = to_dev(inp["x_scales"]).view(torch.float32)
         moe.moe_dispatch(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
                          self.regions.table, self.sregions.table if fp8 else None,
-                         cap_d, lay.workspace, lay.status)
+                         cap_d, lay.workspace, lay.status, scale_pitch=self.scale_pitch)
 
         y = torch.empty((max(1, T), H), dtype=torch.int16, device="cuda")
         y.fill_(0x5A5A)
@@ -87,7 +90,8 @@ class GpuRun:
             moe.moe_expert_scale(self.regions.table,
                                  self.sregions.table if fp8 else None, dtype, H, E, R,
                                  ident, lay.expert_offset, lay.rank_offset, cap_d,
-                                 self.eregions.table, max(1, T * k))
+                                 self.eregions.table, max(1, T * k),
+                                 scale_pitch=self.scale_pitch)
             ey_table = self.eregions.table
         moe.moe_combine(ey_table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, cap_d,
                         y, lay.workspace, lay.status)
@@ -110,7 +114,7 @@ class GpuRun:
 
 
 def oracle_chain(cfg, inp, topk_idx=None, topk_w=None, caps=None, identity=None,
-                 combine_on_dispatch=False):
+                 combine_on_dispatch=False, scale_pitch=0):
     E, R, H = cfg["E"], cfg["R"], cfg["H"]
     idx = inp["topk_idx"] if topk_idx is None else topk_idx
     w = inp["topk_w"] if topk_w is None else topk_w
@@ -120,7 +124,8 @@ def oracle_chain(cfg, inp, topk_idx=None, topk_w=None, caps=None, identity=None,
     cap = lay["rank_count"] if caps is None else caps
     xs = u8_rows(inp["x_scales"]) if fp8 else None
     regs, sregs, st_d = oracle.dispatch(u8_rows(inp["x"]), xs, idx, lay["pos"],
-                                        lay["rank_offset"], E, R, cap, SENTINEL)
+                                        lay["rank_offset"], E, R, cap, SENTINEL,
+                                        scale_pitch=scale_pitch)
     if combine_on_dispatch:
         ey = [r.view(np.uint16).reshape(r.shape[0], H) for r in regs]
     else:

@@ -348,6 +348,28 @@ def pin_dispatch_rows_are_source_rows():
                 assert np.all(sregs[r][n:] == 0xA5)
 
 
+def pin_dispatch_pitched_scale_rows():
+    """Scale rows spaced by a pitch: the scales, then zeros to the pitch; rows
+    never written keep the sentinel."""
+    cfg = wl.custom(80, 640, 16, 4, 3, payload=wl.FP8_E4M3, seed=8)
+    inp = wl.make_inputs(cfg)
+    lay = oracle.layout(inp["topk_idx"], 16, 4)
+    cap = lay["rank_count"] + 1
+    xs = _rows_u8(inp["x_scales"])
+    sb = xs.shape[1]
+    for pitch in (sb, 32, 128):
+        _, sregs, st = oracle.dispatch(_rows_u8(inp["x"]), xs, inp["topk_idx"], lay["pos"],
+                                       lay["rank_offset"], 16, 4, cap, scale_pitch=pitch)
+        assert st == 0
+        for r in range(4):
+            n = int(lay["rank_count"][r])
+            src = lay["row_src"][lay["rank_offset"][r]:lay["rank_offset"][r] + n] // 3
+            assert sregs[r].shape == (int(cap[r]), pitch)
+            assert np.array_equal(sregs[r][:n, :sb], xs[src])
+            assert np.all(sregs[r][:n, sb:] == 0)
+            assert np.all(sregs[r][n:] == 0xA5)
+
+
 def pin_dispatch_capacity_overflow():
     cfg = wl.custom(50, 16, 8, 2, 2, seed=6)
     inp = wl.make_inputs(cfg)
@@ -373,7 +395,7 @@ def _torch_bf16_bits(f32):
         torch.bfloat16).view(torch.int16).numpy().astype(np.uint16)
 
 
-def _end_to_end(cfg, idx, w, identity):
+def _end_to_end(cfg, idx, w, identity, scale_pitch=0):
     inp = wl.make_inputs(cfg)
     E, R, H = cfg["E"], cfg["R"], cfg["H"]
     lay = oracle.layout(idx, E, R)
@@ -381,7 +403,7 @@ def _end_to_end(cfg, idx, w, identity):
     fp8 = cfg["payload"] == wl.FP8_E4M3
     xs = _rows_u8(inp["x_scales"]) if fp8 else None
     regs, sregs, _ = oracle.dispatch(_rows_u8(inp["x"]), xs, idx, lay["pos"],
-                                     lay["rank_offset"], E, R, cap)
+                                     lay["rank_offset"], E, R, cap, scale_pitch=scale_pitch)
     ey = oracle.expert_scale(regs, sregs, fp8, H, E, R, identity,
                              lay["expert_offset"], lay["rank_offset"], cap)
     y, st = oracle.combine(ey, w, idx, lay["pos"], lay["rank_offset"], cap, E, R, H)
@@ -418,11 +440,12 @@ def pin_combine_scaled_closed_form():
     bf16 roundings (expert output and y), bf16 and fp8 payloads.  With all
     weights and scales positive the terms share x's sign, so the relative
     bound holds element-wise."""
-    for cfg in (wl.custom(300, 136, 32, 8, 4, seed=9),
-                wl.custom(100, 256, 16, 4, 3, payload=wl.FP8_E4M3, seed=10)):
+    for cfg, pitch in ((wl.custom(300, 136, 32, 8, 4, seed=9), 0),
+                       (wl.custom(100, 256, 16, 4, 3, payload=wl.FP8_E4M3, seed=10), 0),
+                       (wl.custom(100, 256, 16, 4, 3, payload=wl.FP8_E4M3, seed=10), 128)):
         inp0 = wl.make_inputs(cfg)
         idx, w = inp0["topk_idx"], inp0["topk_w"]
-        inp, _, _, y, st = _end_to_end(cfg, idx, w, False)
+        inp, _, _, y, st = _end_to_end(cfg, idx, w, False, scale_pitch=pitch)
         assert st == 0
         if cfg["payload"] == wl.BF16:
             xf = _bf16_rows_to_f64(inp["x"])

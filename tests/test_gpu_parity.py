@@ -29,15 +29,15 @@ def _h():
 
 
 def _full_parity(cfg, inp=None, idx=None, w=None, spare_rows=2, cap_delta=None,
-                 identity=None):
+                 identity=None, scale_pitch=None):
     h = _h()
     inp = wl.make_inputs(cfg) if inp is None else inp
     h.log(f"[parity] {cfg['name']} T={cfg['T']} H={cfg['H']} E={cfg['E']} R={cfg['R']} "
           f"k={(idx if idx is not None else inp['topk_idx']).shape[1]}")
     run = h.GpuRun(cfg, inp, topk_idx=idx, topk_w=w, spare_rows=spare_rows,
-                   cap_delta=cap_delta, identity=identity)
+                   cap_delta=cap_delta, identity=identity, scale_pitch=scale_pitch)
     ref = h.oracle_chain(cfg, inp, topk_idx=idx, topk_w=w, caps=run.caps,
-                         identity=identity)
+                         identity=identity, scale_pitch=run.scale_pitch)
     # layout: bit-exact
     for key in ("expert_count", "expert_offset", "rank_count", "rank_offset", "pos",
                 "row_src"):
@@ -98,12 +98,34 @@ def test_tiny_identity_softmax_returns_x():
     (400, 128, 16, 16, 4, wl.BF16, 0.0),       # R = E
     (1, 8, 4, 2, 2, wl.BF16, 0.0),             # one token, one 16-byte segment
     (2049, 2048, 256, 64, 8, wl.BF16, 0.0),
+    (256, 512, 32, 8, 4, wl.BF16, 0.1),        # largest single-kernel layout
+    (257, 512, 32, 8, 4, wl.BF16, 0.1),        # smallest two-kernel layout
+    (300, 2048, 16, 4, 2, wl.FP8_E4M3, 0.0),   # 64-byte scale rows
+    (90, 8192, 64, 16, 6, wl.FP8_E4M3, 0.1),   # 256-byte scale rows, k=6
+    (64, 1152, 1024, 256, 8, wl.BF16, 0.0),    # maximum expert count
 ])
 def test_custom_shapes(T, H, E, R, k, payload, mask):
     cfg = wl.custom(T, H, E, R, k, payload=payload, seed=T + H)
     inp = wl.make_inputs(cfg)
     idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
     _full_parity(cfg, inp, idx=idx)
+
+
+@pytest.mark.parametrize("pitch", [0, 116, 128, 256])
+def test_fp8_scale_pitch(pitch):
+    """Scale rows (112 bytes here) packed (pitch 0) or pitched: scales then
+    zeros to the pitch; 116 takes the 4-byte path."""
+    cfg = wl.custom(333, 3584, 64, 16, 8, payload=wl.FP8_E4M3, seed=77)
+    _full_parity(cfg, scale_pitch=pitch)
+
+
+def test_fp8_scale_pitch_too_small_is_rejected():
+    from paper_2607_26444_amd import moe
+    h = _h()
+    cfg = wl.custom(16, 3584, 64, 16, 8, payload=wl.FP8_E4M3, seed=78)
+    with pytest.raises(moe.MoeError) as ei:
+        h.GpuRun(cfg, wl.make_inputs(cfg), scale_pitch=64)
+    assert ei.value.code == moe.MOE_EINVAL
 
 
 def test_all_slots_unused():
@@ -187,7 +209,8 @@ def test_full_size_workloads(name):
     fp8 = cfg["payload"] == wl.FP8_E4M3
     xs = h.u8_rows(inp["x_scales"]) if fp8 else None
     regs, sregs, st = oracle.dispatch(h.u8_rows(inp["x"]), xs, inp["topk_idx"], lay["pos"],
-                                      lay["rank_offset"], E, R, run.caps, h.SENTINEL)
+                                      lay["rank_offset"], E, R, run.caps, h.SENTINEL,
+                                      scale_pitch=run.scale_pitch)
     assert st == 0
     h.check_regions(run, run.regions, regs)
     if fp8:
@@ -201,7 +224,7 @@ def test_full_size_workloads(name):
                x=inp["x"][sample],
                x_scales=inp["x_scales"][sample] if fp8 else None)
     subcfg = dict(cfg, T=len(sample))
-    ref = h.oracle_chain(subcfg, sub)
+    ref = h.oracle_chain(subcfg, sub, scale_pitch=run.scale_pitch)
     ok, msg = h.combine_close(run.y[sample], ref["y"])
     assert ok, msg
     h.log(f"[full] {cfg['name']} sampled combine ok ({msg})")

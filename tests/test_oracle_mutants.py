@@ -45,10 +45,12 @@ MUTANTS = [
     ("plan_boundary_off_by_one", "a[(size_t)t] * P < p * A", "a[(size_t)t] * P <= p * A"),
     ("dispatch_short_copy", "x + t * row_bytes, (size_t)row_bytes);",
      "x + t * row_bytes, (size_t)row_bytes - 2);"),
-    ("dispatch_scales_from_token0", "x_scales + t * scale_row_bytes",
-     "x_scales + 0 * t * scale_row_bytes"),
+    ("dispatch_scales_from_token0", "x_scales + t * scale_row_bytes, (size_t)scale_row_bytes",
+     "x_scales + 0 * t * scale_row_bytes, (size_t)scale_row_bytes"),
     ("expert_scale_off_by_one", "1.0f + 0.01f * (float)e", "1.0f + 0.01f * (float)(e + 1)"),
-    ("expert_fp8_block_zero", "(local * nblk + h / 128) * 4", "(local * nblk + 0 * h) * 4"),
+    ("expert_fp8_block_zero", "local * scale_pitch + (h / 128) * 4", "local * scale_pitch + 0 * h"),
+    ("dispatch_scale_pad_not_zeroed", "for (int64_t b = scale_row_bytes; b < scale_pitch; ++b) srow[b] = 0;",
+     "for (int64_t b = scale_row_bytes; b < scale_pitch; ++b) srow[b] = srow[b];"),
     ("expert_fp8_scale_dropped", "float dq = oracle_fp8e4m3_to_float(in[h]) * sc;",
      "float dq = oracle_fp8e4m3_to_float(in[h]) * (sc > 0 ? 1.0f : 1.0f);"),
     ("combine_drops_weight", "acc[(size_t)h] += w * oracle_bf16_to_double(row[h]);",
