@@ -1,7 +1,7 @@
 """Benchmark of the MoE dispatch/combine hot path on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                [--no-cpu-baseline]
+                [--no-cpu-baseline] [--ablation]
 
 One step = one pass of the whole path on one batch already resident in HBM:
 moe_layout (histograms, scans, placement, partition plan) -> moe_dispatch
@@ -115,6 +115,110 @@ def cpu_baseline(cfg, inp, budget_s=12.0, max_reps=3):
     return float(np.median(times)), len(times)
 
 
+def trace_stats(trace, khz):
+    """Per-wavefront completion times from a (start, end) trace: makespan and
+    the fastest-to-slowest completion gap (Section 9.6 reports this gap per
+    core), relative to the earliest start."""
+    t = trace.view(-1, 2).cpu().numpy().astype(np.int64)
+    t = t[t[:, 0] != 0]
+    t0 = t[:, 0].min()
+    done = (t[:, 1] - t0) / khz * 1e3          # microseconds
+    busy = (t[:, 1] - t[:, 0]) / khz * 1e3
+    return dict(waves=int(len(t)), makespan_us=round(float(done.max()), 2),
+                completion_gap_pct=round(100 * float((done.max() - done.min()) / done.max()), 1),
+                completion_p10_us=round(float(np.percentile(done, 10)), 2),
+                completion_p90_us=round(float(np.percentile(done, 90)), 2),
+                busy_mean_us=round(float(busy.mean()), 2))
+
+
+def ablation(a):
+    """Dispatch under the three work splits of moe_dispatch_ex on one
+    workload: kernel time (HIP events) and the per-wavefront completion trace.
+    One JSON line."""
+    import torch
+    import workloads as wl
+    from paper_2607_26444_amd import moe
+
+    cfg = wl.get(a.workload)
+    T, H, E, R, k = cfg["T"], cfg["H"], cfg["E"], cfg["R"], cfg["k"]
+    fp8 = cfg["payload"] == wl.FP8_E4M3
+    dtype = moe.MOE_DTYPE_FP8_E4M3 if fp8 else moe.MOE_DTYPE_BF16
+    inp = wl.make_inputs(cfg)
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+    x_d = torch.from_numpy(np.ascontiguousarray(inp["x"]).view(np.uint8)).to(dev)
+    xs_d = torch.from_numpy(inp["x_scales"]).to(dev) if fp8 else None
+    idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
+    lay = moe.Layout(T, k, E, R)
+    lay.run(idx_d)
+    torch.cuda.synchronize()
+    rows = [max(1, int(c)) for c in lay.rank_count.cpu().numpy()]
+    sb = wl.scale_row_bytes(cfg)
+    spitch = (sb + 127) // 128 * 128
+    regions = moe.Regions(rows, wl.row_bytes(cfg))
+    sregions = moe.Regions(rows, spitch) if fp8 else None
+    trace = torch.zeros(2 * moe.MOE_PLAN_PARTS, dtype=torch.int64, device=dev)
+    khz = moe.moe_wall_clock_khz()
+    out = {"metric": "dispatch work-split ablation", "config": {"workload": cfg["name"]},
+           "rank_rows_max_over_mean": round(max(rows) / (sum(rows) / len(rows)), 2),
+           "wall_clock_khz": khz, "policies": {}}
+    b = algorithmic_bytes(cfg)
+    for name, pol in (("balanced_push", moe.MOE_POLICY_BALANCED),
+                      ("dynamic_push", moe.MOE_POLICY_DYNAMIC),
+                      ("rows_pull", moe.MOE_POLICY_ROWS),
+                      ("by_rank_pull", moe.MOE_POLICY_BY_RANK)):
+        def run(tr=None):
+            moe.moe_dispatch_ex(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                                lay.row_src, regions.table,
+                                sregions.table if fp8 else None, regions.cap, lay.workspace,
+                                lay.status, policy=pol, trace=tr, scale_pitch=spitch)
+        for _ in range(3):
+            run()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(a.steps):
+            run()
+        e1.record(stream)
+        trace.zero_()
+        run(trace)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / a.steps
+        rec = dict(dispatch_us=round(us, 2), GBps=round(b["dispatch"] / (us * 1e-6) / 1e9, 1))
+        rec.update(trace_stats(trace, khz))
+        out["policies"][name] = rec
+        print(f"[ablation] {name}: {rec}", file=sys.stderr, flush=True)
+    # combine: static vs dynamic part assignment (expert outputs = the rows)
+    w_d = torch.from_numpy(inp["topk_w"]).to(dev)
+    if not fp8:
+        y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        out["combine"] = {}
+        for name, pol in (("balanced", moe.MOE_POLICY_BALANCED),
+                          ("dynamic", moe.MOE_POLICY_DYNAMIC)):
+            def runc(tr=None):
+                moe.moe_combine_ex(regions.table, w_d, H, E, R, idx_d, lay.pos,
+                                   lay.rank_offset, regions.cap, y, lay.workspace, lay.status,
+                                   policy=pol, trace=tr)
+            for _ in range(3):
+                runc()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(a.steps):
+                runc()
+            e1.record(stream)
+            trace.zero_()
+            runc(trace)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / a.steps
+            rec = dict(combine_us=round(us, 2), GBps=round(b["combine"] / (us * 1e-6) / 1e9, 1))
+            rec.update(trace_stats(trace, khz))
+            out["combine"][name] = rec
+            print(f"[ablation] combine {name}: {rec}", file=sys.stderr, flush=True)
+    st = int(lay.status.item())
+    out["status"] = st
+    print(json.dumps(out), flush=True)
+    return 0 if st == 0 else 1
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,11 +226,16 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="prefill")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the step benchmark: dispatch under each work split")
     a = ap.parse_args(argv)
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the operator; runs on more than "
               "one GPU are not part of this build (use --gpus 1).", file=sys.stderr)
         return 2
+
+    if a.ablation:
+        return ablation(a)
 
     import torch
     import workloads as wl

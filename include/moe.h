@@ -95,6 +95,10 @@ const char* moe_strerror(int code);
  * none). */
 int moe_last_hip_error(void);
 
+/* Rate of the clock the trace buffers of moe_dispatch_ex / moe_combine_ex
+ * use on the current device, in kHz (written to *khz, a HOST pointer). */
+int moe_wall_clock_khz(int* khz);
+
 /*
  * moe_layout_workspace_bytes -- device workspace that moe_layout needs for
  * a batch of this shape (written to *out_bytes, a HOST pointer).  The
@@ -167,6 +171,40 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
                  const void* workspace, size_t workspace_bytes, uint32_t* status,
                  void* stream);
 
+/* Work-split policies of moe_dispatch_ex (all give bit-identical regions). */
+#define MOE_POLICY_BALANCED 0 /* byte-balanced token ranges, push (moe_dispatch) */
+#define MOE_POLICY_ROWS 1     /* pull: the N routed rows split evenly over wavefronts */
+#define MOE_POLICY_BY_RANK 2  /* pull: a fixed group of W/R wavefronts per rank */
+#define MOE_POLICY_DYNAMIC 3  /* push; byte-balanced parts handed out at run time */
+
+/*
+ * moe_dispatch_ex -- moe_dispatch with a choice of work split and an
+ * optional per-wavefront trace; for studying the partitioning of Section 6.2
+ * (Section 9.6 compares a naive per-peer core assignment with the balanced
+ * one; MOE_POLICY_BY_RANK is that naive assignment, MOE_POLICY_ROWS splits
+ * the same pull work evenly, MOE_POLICY_BALANCED is the product path).
+ *
+ * policy       one of MOE_POLICY_*; anything else is MOE_EINVAL.  With
+ *              MOE_POLICY_DYNAMIC each wavefront starts with one part of the
+ *              plan and then claims the next unclaimed part from a counter in
+ *              the workspace (moe_layout zeroes it; the last wavefront resets
+ *              it), so faster wavefronts take more parts.  Calls that share a
+ *              workspace must not run concurrently under this policy.
+ * trace        NULL, or a device buffer of 2*trace_waves uint64: wavefront g
+ *              (g < trace_waves) writes trace[2g] = its start time and
+ *              trace[2g+1] = the time its last store completed, both from the
+ *              GPU's constant-rate wall clock (hipDeviceAttributeWallClockRate
+ *              kHz).  The launch uses at most MOE_PLAN_PARTS wavefronts;
+ *              entries of wavefronts that do not exist are left untouched.
+ * Other arguments, results and errors are those of moe_dispatch.
+ */
+int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, int H,
+                    int k, int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                    const int32_t* rank_offset, const int32_t* row_src, const uint64_t* recv_x,
+                    const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
+                    const void* workspace, size_t workspace_bytes, uint32_t* status,
+                    int policy, uint64_t* trace, int trace_waves, void* stream);
+
 /*
  * moe_combine -- gather each token's expert outputs back to token order and
  * reduce them with the top-k weights (Section 6.1: operands are loaded and
@@ -187,6 +225,17 @@ int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H,
                 const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
                 const void* workspace, size_t workspace_bytes, uint32_t* status,
                 void* stream);
+
+/*
+ * moe_combine_ex -- moe_combine with a work split (MOE_POLICY_BALANCED or
+ * MOE_POLICY_DYNAMIC, as for moe_dispatch_ex; others are MOE_EINVAL) and the
+ * optional per-wavefront trace of moe_dispatch_ex (same layout and clock).
+ */
+int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
+                   int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                   const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
+                   const void* workspace, size_t workspace_bytes, uint32_t* status,
+                   int policy, uint64_t* trace, int trace_waves, void* stream);
 
 /*
  * moe_expert_scale -- stand-in expert for tests and benchmarks, not part of

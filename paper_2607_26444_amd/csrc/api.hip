@@ -77,6 +77,14 @@ const char* moe_strerror(int code) {
 
 int moe_last_hip_error(void) { return g_last_hip_error; }
 
+int moe_wall_clock_khz(int* khz) {
+  if (!khz) return MOE_EINVAL;
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err == hipSuccess) err = hipDeviceGetAttribute(khz, hipDeviceAttributeWallClockRate, dev);
+  return launched(err);
+}
+
 int moe_layout_workspace_bytes(int64_t T, int k, int E, int R, size_t* out_bytes) {
   if (!out_bytes) return MOE_EINVAL;
   const int rc = shape_ok(T, k, E, R);
@@ -101,11 +109,12 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R, int32_t*
                                      as_stream(stream)));
 }
 
-int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k, int E,
-                 int R, const int32_t* topk_idx, const int32_t* pos, const int32_t* rank_offset,
-                 const uint64_t* recv_x, const uint64_t* recv_scales, int scale_pitch,
-                 const int32_t* recv_cap, const void* workspace, size_t workspace_bytes,
-                 uint32_t* status, void* stream) {
+int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,
+                    int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                    const int32_t* rank_offset, const int32_t* row_src, const uint64_t* recv_x,
+                    const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
+                    const void* workspace, size_t workspace_bytes, uint32_t* status,
+                    int policy, uint64_t* trace, int trace_waves, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1 || (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3)) return MOE_EINVAL;
@@ -113,6 +122,12 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
   if (!recv_x || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
   if (fp8 && (!x_scales || !recv_scales)) return MOE_EINVAL;
   if (T > 0 && (!x || !topk_idx || !pos)) return MOE_EINVAL;
+  if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_ROWS &&
+      policy != MOE_POLICY_BY_RANK && policy != MOE_POLICY_DYNAMIC)
+    return MOE_EINVAL;
+  const bool pull = policy == MOE_POLICY_ROWS || policy == MOE_POLICY_BY_RANK;
+  if (pull && T > 0 && !row_src) return MOE_EINVAL;
+  if (trace && trace_waves < 0) return MOE_EINVAL;
   const int64_t row_bytes = fp8 ? (int64_t)H : 2 * (int64_t)H;
   if (row_bytes % 16 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
   if (!aligned(x, 16) || (fp8 && !aligned(x_scales, 4))) return MOE_EALIGN;
@@ -139,18 +154,37 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
   a.recv_cap = recv_cap;
   a.bound = static_cast<const int32_t*>(workspace);
   a.status = status;
-  return launched(moe::launch_dispatch(a, as_stream(stream)));
+  a.row_src = row_src;
+  a.R = R;
+  a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
+                                          moe::layout_geom(T, E).ticket_offset);
+  a.trace = trace;
+  a.trace_waves = trace ? trace_waves : 0;
+  return launched(moe::launch_dispatch(a, policy, as_stream(stream)));
 }
 
-int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k, int E,
-                int R, const int32_t* topk_idx, const int32_t* pos, const int32_t* rank_offset,
-                const int32_t* recv_cap, uint16_t* y, const void* workspace,
-                size_t workspace_bytes, uint32_t* status, void* stream) {
+int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k, int E,
+                 int R, const int32_t* topk_idx, const int32_t* pos, const int32_t* rank_offset,
+                 const uint64_t* recv_x, const uint64_t* recv_scales, int scale_pitch,
+                 const int32_t* recv_cap, const void* workspace, size_t workspace_bytes,
+                 uint32_t* status, void* stream) {
+  return moe_dispatch_ex(x, x_scales, dtype, T, H, k, E, R, topk_idx, pos, rank_offset, nullptr,
+                         recv_x, recv_scales, scale_pitch, recv_cap, workspace, workspace_bytes,
+                         status, MOE_POLICY_BALANCED, nullptr, 0, stream);
+}
+
+int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
+                   int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                   const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
+                   const void* workspace, size_t workspace_bytes, uint32_t* status,
+                   int policy, uint64_t* trace, int trace_waves, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1) return MOE_EINVAL;
   if (!expert_y || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
   if (T > 0 && (!topk_w || !topk_idx || !pos || !y)) return MOE_EINVAL;
+  if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_DYNAMIC) return MOE_EINVAL;
+  if (trace && trace_waves < 0) return MOE_EINVAL;
   if ((2 * (int64_t)H) % 16 != 0 || !aligned(y, 16)) return MOE_EALIGN;
   if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
     return MOE_EWORKSPACE;
@@ -168,7 +202,20 @@ int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H,
   a.y = y;
   a.bound = static_cast<const int32_t*>(workspace);
   a.status = status;
-  return launched(moe::launch_combine(a, as_stream(stream)));
+  a.trace = trace;
+  a.trace_waves = trace ? trace_waves : 0;
+  a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
+                                          moe::layout_geom(T, E).ticket_offset) + 2;
+  return launched(moe::launch_combine(a, policy, as_stream(stream)));
+}
+
+int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k, int E,
+                int R, const int32_t* topk_idx, const int32_t* pos, const int32_t* rank_offset,
+                const int32_t* recv_cap, uint16_t* y, const void* workspace,
+                size_t workspace_bytes, uint32_t* status, void* stream) {
+  return moe_combine_ex(expert_y, topk_w, T, H, k, E, R, topk_idx, pos, rank_offset, recv_cap, y,
+                        workspace, workspace_bytes, status, MOE_POLICY_BALANCED, nullptr, 0,
+                        stream);
 }
 
 int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int scale_pitch,

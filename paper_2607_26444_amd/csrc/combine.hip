@@ -98,7 +98,7 @@ __device__ __forceinline__ void combine_row(uint8_t* dst, const uint8_t* const (
 }
 
 // KW: slots resolved per token (>= k).
-template <int KW>
+template <int KW, bool DYN>
 __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
   // Per-slot source row and weight of the current batch, one entry per lane
   // of each wavefront (0 = slot not combined), padded with zeros so a token
@@ -108,7 +108,9 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
   const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
-  const int t0 = a.bound[g * a.parts_per_wave], t1 = a.bound[(g + 1) * a.parts_per_wave];
+  const uint64_t t_start = a.trace ? (uint64_t)wall_clock64() : 0;
+  const int W = gridDim.x * kWavesPerBlock;
+  const int m = DYN ? 1 : a.parts_per_wave;  // plan parts per unit of work
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t l16 = lane * kVecBytes;
   const int k = a.k;
@@ -121,6 +123,9 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
     s_w[wv][kWave + lane] = 0.0f;
   }
 
+  for (int chunk = g; chunk * m < MOE_PLAN_PARTS;
+       chunk = DYN ? next_chunk<DYN>(a.tickets, W, lane) : MOE_PLAN_PARTS) {
+  const int t0 = a.bound[chunk * m], t1 = a.bound[(chunk + 1) * m];
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t srow = 0;
@@ -177,30 +182,39 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
       }
     }
   }
+  }
+  finish_chunks<DYN>(a.tickets, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
+  trace_wave(a.trace, a.trace_waves, g, t_start, lane);
 }
 
-template <int KW>
+template <int KW, bool DYN>
 hipError_t launch_kw(CombineArgs a, hipStream_t stream) {
-  const void* fn = reinterpret_cast<const void*>(&combine_kernel<KW>);
+  const void* fn = reinterpret_cast<const void*>(&combine_kernel<KW, DYN>);
   const int waves = resident_waves(fn, 0);
   a.parts_per_wave = MOE_PLAN_PARTS / waves;
-  hipLaunchKernelGGL((combine_kernel<KW>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
+  hipLaunchKernelGGL((combine_kernel<KW, DYN>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
                      stream, a);
   return hipGetLastError();
 }
 
+template <bool DYN>
+hipError_t launch_dyn(const CombineArgs& a, hipStream_t stream) {
+  switch (slot_width(a.k)) {
+    case 2: return launch_kw<2, DYN>(a, stream);
+    case 4: return launch_kw<4, DYN>(a, stream);
+    case 8: return launch_kw<8, DYN>(a, stream);
+    case 16: return launch_kw<16, DYN>(a, stream);
+    default: return launch_kw<32, DYN>(a, stream);
+  }
+}
+
 }  // namespace
 
-hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
-  switch (slot_width(a.k)) {
-    case 2: return launch_kw<2>(a, stream);
-    case 4: return launch_kw<4>(a, stream);
-    case 8: return launch_kw<8>(a, stream);
-    case 16: return launch_kw<16>(a, stream);
-    default: return launch_kw<32>(a, stream);
-  }
+hipError_t launch_combine(const CombineArgs& a, int policy, hipStream_t stream) {
+  return policy == MOE_POLICY_DYNAMIC ? launch_dyn<true>(a, stream)
+                                      : launch_dyn<false>(a, stream);
 }
 
 }  // namespace moe

@@ -26,7 +26,7 @@ namespace {
 
 // VPL: 1 KiB segments held per lane-set (row bytes up to VPL KiB per pass).
 // FULL: row bytes == VPL KiB exactly (no per-lane tail test).
-template <int VPL, bool FULL, bool SCALES>
+template <int VPL, bool FULL, bool SCALES, bool DYN>
 __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
   // Destination row (and scale row) of every slot of the current batch, one
   // entry per lane of each wavefront (0 = slot not dispatched), padded with
@@ -36,7 +36,9 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
   const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
-  const int t0 = a.bound[g * a.parts_per_wave], t1 = a.bound[(g + 1) * a.parts_per_wave];
+  const uint64_t t_start = a.trace ? (uint64_t)wall_clock64() : 0;
+  const int W = gridDim.x * kWavesPerBlock;
+  const int m = DYN ? 1 : a.parts_per_wave;  // plan parts per unit of work
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t sb = (uint32_t)a.scale_row_bytes;
   const uint32_t sp = (uint32_t)a.scale_pitch;
@@ -51,6 +53,9 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     if (SCALES) s_sdst[wv][kWave + lane] = 0;
   }
 
+  for (int chunk = g; chunk * m < MOE_PLAN_PARTS;
+       chunk = DYN ? next_chunk<DYN>(a.tickets, W, lane) : MOE_PLAN_PARTS) {
+  const int t0 = a.bound[chunk * m], t1 = a.bound[(chunk + 1) * m];
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t dst = 0, sdst = 0;
@@ -118,52 +123,188 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
       }
     }
   }
+  }
+  finish_chunks<DYN>(a.tickets, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
+  trace_wave(a.trace, a.trace_waves, g, t_start, lane);
 }
 
+// Pull dispatch for the partitioning study: a wavefront walks a range of
+// global (destination) rows and pulls each row's source token from x.
+// POLICY MOE_POLICY_ROWS: the N routed rows are split evenly over the W
+// wavefronts.  MOE_POLICY_BY_RANK: wavefronts form R fixed groups of W/R
+// and group r splits rank r's rows (a per-peer core assignment that ignores
+// how many rows each rank receives).  Per batch of 64 rows, lane l resolves
+// row ib+l (source row, destination) into LDS, as the push kernel does.
+template <int VPL, bool FULL, bool SCALES, int POLICY>
+__global__ __launch_bounds__(kBlock) void dispatch_pull_kernel(DispatchArgs a) {
+  __shared__ uint64_t s_src[kWavesPerBlock][kWave];
+  __shared__ uint64_t s_dst[kWavesPerBlock][kWave];
+  __shared__ uint64_t s_ssrc[kWavesPerBlock][SCALES ? kWave : 1];
+  __shared__ uint64_t s_sdst[kWavesPerBlock][SCALES ? kWave : 1];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = threadIdx.x / kWave;
+  const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
+  const uint64_t t_start = a.trace ? (uint64_t)wall_clock64() : 0;
+  const int W = gridDim.x * kWavesPerBlock;
+  const uint32_t rb = (uint32_t)a.row_bytes;
+  const uint32_t sb = (uint32_t)a.scale_row_bytes;
+  const uint32_t sp = (uint32_t)a.scale_pitch;
+  const uint32_t l16 = lane * kVecBytes;
+  int64_t i0 = 0, i1 = 0;
+  if (POLICY == MOE_POLICY_ROWS) {
+    const int64_t n = a.rank_offset[a.R];
+    i0 = n * g / W;
+    i1 = n * (g + 1) / W;
+  } else {
+    const int G = W / a.R;  // the launch makes W a multiple of R
+    const int r = g / G, q = g - r * G;
+    if (r < a.R) {
+      const int64_t b = a.rank_offset[r], n = a.rank_offset[r + 1] - b;
+      i0 = b + n * q / G;
+      i1 = b + n * (q + 1) / G;
+    }
+  }
+  uint32_t st = 0;
+  for (int64_t ib = i0; ib < i1; ib += kWave) {
+    const int64_t ie = min(i1, ib + kWave);
+    uint64_t src = 0, dst = 0, ssrc = 0, sdst = 0;
+    if (ib + lane < ie) {
+      const int64_t i = ib + lane;
+      const int s = a.row_src[i];
+      const int t = s / a.k;
+      const int r = a.topk_idx[s] / a.L;
+      const int64_t local = i - a.rank_offset[r];
+      if (local >= 0 && local < a.recv_cap[r]) {
+        src = reinterpret_cast<uint64_t>(a.x) + (uint64_t)t * rb;
+        dst = a.recv_x[r] + (uint64_t)local * rb;
+        if (SCALES) {
+          ssrc = reinterpret_cast<uint64_t>(a.x_scales) + (uint64_t)t * sb;
+          sdst = a.recv_scales[r] + (uint64_t)local * sp;
+        }
+      } else {
+        st |= MOE_STATUS_CAPACITY;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    s_src[wv][lane] = src;
+    s_dst[wv][lane] = dst;
+    if (SCALES) {
+      s_ssrc[wv][lane] = ssrc;
+      s_sdst[wv][lane] = sdst;
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int l = 0; l < (int)(ie - ib); ++l) {
+      const uint8_t* sr = reinterpret_cast<const uint8_t*>(readlane64(s_src[wv][l], 0));
+      uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(s_dst[wv][l], 0));
+      if (!d) continue;
+      for (uint32_t seg = 0; seg < rb; seg += VPL * kWaveBytes) {
+        u32x4 v[VPL];
+#pragma unroll
+        for (int c = 0; c < VPL; ++c) {
+          const uint32_t off = seg + c * kWaveBytes + l16;
+          if (FULL || off < rb) v[c] = ld16(sr + off);
+        }
+#pragma unroll
+        for (int c = 0; c < VPL; ++c) {
+          const uint32_t off = seg + c * kWaveBytes + l16;
+          if (FULL || off < rb) st16(d + off, v[c]);
+        }
+      }
+      if (SCALES) {
+        const uint8_t* ss = reinterpret_cast<const uint8_t*>(readlane64(s_ssrc[wv][l], 0));
+        uint8_t* sd = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l], 0));
+        for (uint32_t o = 0; o < sp; o += kWave * 4) {
+          const uint32_t off = o + lane * 4;
+          uint32_t s4 = 0;
+          if (off < sb) s4 = ld4(ss + off);
+          if (off < sp) st4(sd + off, s4);
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  st = wave_or(st);
+  if (st && lane == 0) atomicOr(a.status, st);
+  trace_wave(a.trace, a.trace_waves, g, t_start, lane);
+}
+
+template <int VPL, bool FULL, bool SCALES, int POLICY>
+hipError_t launch_pull(DispatchArgs a, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&dispatch_pull_kernel<VPL, FULL, SCALES, POLICY>);
+  int waves = resident_waves(fn, 0);
+  if (POLICY == MOE_POLICY_BY_RANK) {
+    // whole groups per rank, and whole workgroups
+    waves = waves / a.R * a.R;
+    while (waves > a.R && waves % kWavesPerBlock != 0) waves -= a.R;
+    if (waves < a.R || waves % kWavesPerBlock != 0) waves = a.R * kWavesPerBlock;
+  }
+  hipLaunchKernelGGL((dispatch_pull_kernel<VPL, FULL, SCALES, POLICY>),
+                     dim3(waves / kWavesPerBlock), dim3(kBlock), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int VPL, bool SCALES, bool DYN>
+hipError_t launch_push(DispatchArgs a, hipStream_t stream);
+
 template <int VPL, bool SCALES>
-hipError_t launch_vpl(DispatchArgs a, hipStream_t stream) {
+hipError_t launch_vpl(DispatchArgs a, int policy, hipStream_t stream) {
   const bool full = a.row_bytes == (int64_t)VPL * kWaveBytes;
-  const void* fn = full ? reinterpret_cast<const void*>(&dispatch_kernel<VPL, true, SCALES>)
-                        : reinterpret_cast<const void*>(&dispatch_kernel<VPL, false, SCALES>);
+  if (policy == MOE_POLICY_ROWS)
+    return full ? launch_pull<VPL, true, SCALES, MOE_POLICY_ROWS>(a, stream)
+                : launch_pull<VPL, false, SCALES, MOE_POLICY_ROWS>(a, stream);
+  if (policy == MOE_POLICY_BY_RANK)
+    return full ? launch_pull<VPL, true, SCALES, MOE_POLICY_BY_RANK>(a, stream)
+                : launch_pull<VPL, false, SCALES, MOE_POLICY_BY_RANK>(a, stream);
+  if (policy == MOE_POLICY_DYNAMIC) return launch_push<VPL, SCALES, true>(a, stream);
+  return launch_push<VPL, SCALES, false>(a, stream);
+}
+
+template <int VPL, bool SCALES, bool DYN>
+hipError_t launch_push(DispatchArgs a, hipStream_t stream) {
+  const bool full = a.row_bytes == (int64_t)VPL * kWaveBytes;
+  const void* fn =
+      full ? reinterpret_cast<const void*>(&dispatch_kernel<VPL, true, SCALES, DYN>)
+           : reinterpret_cast<const void*>(&dispatch_kernel<VPL, false, SCALES, DYN>);
   const int waves = resident_waves(fn, 0);
   a.parts_per_wave = MOE_PLAN_PARTS / waves;
   const dim3 grid(waves / kWavesPerBlock), block(kBlock);
   if (full)
-    hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES, DYN>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((dispatch_kernel<VPL, false, SCALES>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((dispatch_kernel<VPL, false, SCALES, DYN>), grid, block, 0, stream, a);
   return hipGetLastError();
 }
 
 template <bool SCALES>
-hipError_t launch_scales(const DispatchArgs& a, hipStream_t stream) {
+hipError_t launch_scales(const DispatchArgs& a, int policy, hipStream_t stream) {
   const int64_t segs = (a.row_bytes + kWaveBytes - 1) / kWaveBytes;
   switch (segs) {
-    case 1: return launch_vpl<1, SCALES>(a, stream);
-    case 2: return launch_vpl<2, SCALES>(a, stream);
-    case 3: return launch_vpl<3, SCALES>(a, stream);
-    case 4: return launch_vpl<4, SCALES>(a, stream);
-    case 5: return launch_vpl<5, SCALES>(a, stream);
-    case 6: return launch_vpl<6, SCALES>(a, stream);
-    case 7: return launch_vpl<7, SCALES>(a, stream);
-    case 8: return launch_vpl<8, SCALES>(a, stream);
-    case 9: return launch_vpl<9, SCALES>(a, stream);
-    case 10: return launch_vpl<10, SCALES>(a, stream);
-    case 11: return launch_vpl<11, SCALES>(a, stream);
-    case 12: return launch_vpl<12, SCALES>(a, stream);
-    case 13: return launch_vpl<13, SCALES>(a, stream);
-    case 14: return launch_vpl<14, SCALES>(a, stream);
-    case 15: return launch_vpl<15, SCALES>(a, stream);
-    default: return launch_vpl<kMaxSegVecs, SCALES>(a, stream);
+    case 1: return launch_vpl<1, SCALES>(a, policy, stream);
+    case 2: return launch_vpl<2, SCALES>(a, policy, stream);
+    case 3: return launch_vpl<3, SCALES>(a, policy, stream);
+    case 4: return launch_vpl<4, SCALES>(a, policy, stream);
+    case 5: return launch_vpl<5, SCALES>(a, policy, stream);
+    case 6: return launch_vpl<6, SCALES>(a, policy, stream);
+    case 7: return launch_vpl<7, SCALES>(a, policy, stream);
+    case 8: return launch_vpl<8, SCALES>(a, policy, stream);
+    case 9: return launch_vpl<9, SCALES>(a, policy, stream);
+    case 10: return launch_vpl<10, SCALES>(a, policy, stream);
+    case 11: return launch_vpl<11, SCALES>(a, policy, stream);
+    case 12: return launch_vpl<12, SCALES>(a, policy, stream);
+    case 13: return launch_vpl<13, SCALES>(a, policy, stream);
+    case 14: return launch_vpl<14, SCALES>(a, policy, stream);
+    case 15: return launch_vpl<15, SCALES>(a, policy, stream);
+    default: return launch_vpl<kMaxSegVecs, SCALES>(a, policy, stream);
   }
 }
 
 }  // namespace
 
-hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t stream) {
-  return a.x_scales ? launch_scales<true>(a, stream) : launch_scales<false>(a, stream);
+hipError_t launch_dispatch(const DispatchArgs& a, int policy, hipStream_t stream) {
+  return a.x_scales ? launch_scales<true>(a, policy, stream)
+                    : launch_scales<false>(a, policy, stream);
 }
 
 }  // namespace moe

@@ -136,7 +136,8 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     int nc, int ncp, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
     int32_t* __restrict__ expert_offset, int32_t* __restrict__ rank_count,
     int32_t* __restrict__ rank_offset, int32_t* __restrict__ pos,
-    int32_t* __restrict__ row_src, int32_t* __restrict__ bound, uint32_t* __restrict__ status) {
+    int32_t* __restrict__ row_src, int32_t* __restrict__ bound, uint32_t* __restrict__ tickets,
+    uint32_t* __restrict__ status) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* mask = reinterpret_cast<uint64_t*>(smem);               // [4][E]
   int64_t* scan = reinterpret_cast<int64_t*>(mask + kWavesPerBlock * E);  // [4]
@@ -233,6 +234,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       rank_offset[R] = (int32_t)n_total;
       bound[0] = 0;
     }
+    if (tid < 4) tickets[tid] = 0u;  // work tickets of dispatch and combine
     for (int r = tid; r < R; r += kBlock) {
       rank_offset[r] = eoff[r * L];
       rank_count[r] = eoff[(r + 1) * L] - eoff[r * L];
@@ -323,14 +325,16 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
                             hipStream_t stream) {
   const LayoutGeom g = layout_geom(T, E);
   int32_t* bound = reinterpret_cast<int32_t*>(workspace);
-  int32_t* counts = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + g.plan_bytes);
+  int32_t* counts = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + g.counts_offset);
+  uint32_t* tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + g.ticket_offset);
   const size_t lds_count = (size_t)kWavesPerBlock * E * 8 + (size_t)E * 4;
   const size_t lds_place = (size_t)kWavesPerBlock * E * 8 + kWavesPerBlock * 8 +
                            (size_t)E * 4 + (size_t)(E + 1) * 4;
   if (g.nc == 1 && T <= kBlock) {
     hipLaunchKernelGGL((layout_place_kernel<KW, true>), dim3(1), dim3(kBlock), lds_place, stream,
                        idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
-                       expert_offset, rank_count, rank_offset, pos, row_src, bound, status);
+                       expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
+                       status);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(layout_count_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_count, stream,
@@ -339,7 +343,8 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL((layout_place_kernel<KW, false>), dim3(g.nc), dim3(kBlock), lds_place,
                      stream, idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
-                     expert_offset, rank_count, rank_offset, pos, row_src, bound, status);
+                     expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
+                     status);
   return hipGetLastError();
 }
 
@@ -355,8 +360,10 @@ LayoutGeom layout_geom(int64_t T, int E) {
   if (g.nc < 1) g.nc = 1;
   g.ncp = (g.nc + 3) / 4 * 4;
   g.plan_bytes = ((size_t)(MOE_PLAN_PARTS + 1) * 4 + 255) / 256 * 256;
+  g.ticket_offset = g.plan_bytes;
+  g.counts_offset = g.ticket_offset + 256;
   g.counts_bytes = (size_t)g.ncp * E * 4;
-  g.total = g.plan_bytes + (g.counts_bytes + 255) / 256 * 256;
+  g.total = g.counts_offset + (g.counts_bytes + 255) / 256 * 256;
   return g;
 }
 

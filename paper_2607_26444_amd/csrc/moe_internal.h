@@ -27,6 +27,8 @@ struct LayoutGeom {
   int nc;
   int ncp;              // nc rounded up to a multiple of 4
   size_t plan_bytes;    // bound[MOE_PLAN_PARTS + 1], padded to 256 bytes
+  size_t ticket_offset; // 4 uint32 work tickets (dispatch next/done, combine next/done)
+  size_t counts_offset;
   size_t counts_bytes;  // int32 [E][ncp], expert-major
   size_t total;
 };
@@ -66,9 +68,14 @@ struct DispatchArgs {
   const int32_t* bound;        // plan: bound[MOE_PLAN_PARTS + 1]
   int32_t parts_per_wave;      // MOE_PLAN_PARTS / launched wavefronts
   uint32_t* status;
+  const int32_t* row_src;      // pull policies only
+  int32_t R;
+  uint32_t* tickets;           // dynamic policy: {next, done}, zeroed by the layout
+  uint64_t* trace;             // optional per-wavefront (start, end) times
+  int32_t trace_waves;
 };
 
-hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t stream);
+hipError_t launch_dispatch(const DispatchArgs& a, int policy, hipStream_t stream);
 
 struct CombineArgs {
   const uint64_t* expert_y;
@@ -84,9 +91,12 @@ struct CombineArgs {
   const int32_t* bound;
   int32_t parts_per_wave;
   uint32_t* status;
+  uint64_t* trace;
+  int32_t trace_waves;
+  uint32_t* tickets;           // dynamic policy: {next, done}, zeroed by the layout
 };
 
-hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, int policy, hipStream_t stream);
 
 struct ExpertArgs {
   const uint64_t* recv_x;
@@ -141,6 +151,42 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
 
 __device__ __forceinline__ float readlane_f32(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// Next unit of work for a wavefront.  Static: one contiguous run of plan
+// parts per wavefront.  Dynamic: a wavefront starts with part g and then
+// takes the next unclaimed part from a ticket counter (no waiting on other
+// wavefronts); the last wavefront to finish resets the counters for the next
+// launch.
+template <bool DYN>
+__device__ __forceinline__ int next_chunk(uint32_t* tickets, int W, int lane) {
+  int nxt = 0;
+  if (DYN && lane == 0) nxt = (int)atomicAdd(&tickets[0], 1u);
+  return W + __builtin_amdgcn_readfirstlane(nxt);
+}
+
+template <bool DYN>
+__device__ __forceinline__ void finish_chunks(uint32_t* tickets, int W, int lane) {
+  if (DYN && lane == 0) {
+    if (atomicAdd(&tickets[1], 1u) == (uint32_t)(W - 1)) {
+      tickets[0] = 0u;
+      tickets[1] = 0u;
+    }
+  }
+}
+
+// Per-wavefront trace record (start, end) in the constant-rate wall clock.
+// The end stamp is taken after the wavefront's stores have completed.
+__device__ __forceinline__ void trace_wave(uint64_t* trace, int trace_waves, int g,
+                                           uint64_t t_start, int lane) {
+  if (trace && g < trace_waves) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    const uint64_t t_end = (uint64_t)wall_clock64();
+    if (lane == 0) {
+      trace[2 * g] = t_start;
+      trace[2 * g + 1] = t_end;
+    }
+  }
 }
 
 __device__ __forceinline__ uint32_t wave_or(uint32_t v) {

@@ -34,10 +34,15 @@ MOE_MAX_EXPERTS = 1024
 MOE_FP8_BLOCK = 128
 MOE_PLAN_PARTS = 12288
 
+MOE_POLICY_BALANCED = 0
+MOE_POLICY_ROWS = 1
+MOE_POLICY_BY_RANK = 2
+MOE_POLICY_DYNAMIC = 3
+
 # Entry points declared in include/moe.h.
-EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error",
+EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error", "moe_wall_clock_khz",
            "moe_layout_workspace_bytes", "moe_layout", "moe_dispatch",
-           "moe_combine", "moe_expert_scale")
+           "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale")
 
 _lib = None
 P = ctypes.c_void_p
@@ -68,14 +73,20 @@ def lib() -> ctypes.CDLL:
         L.moe_strerror.argtypes = [I32]
         L.moe_strerror.restype = ctypes.c_char_p
         L.moe_last_hip_error.restype = I32
+        L.moe_wall_clock_khz.argtypes = [ctypes.POINTER(I32)]
+        L.moe_wall_clock_khz.restype = I32
         L.moe_layout_workspace_bytes.argtypes = [I64, I32, I32, I32, ctypes.POINTER(SZ)]
         L.moe_layout.argtypes = [P, I64, I32, I32, I32, P, P, P, P, P, P, P, SZ, P, P]
         L.moe_dispatch.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, I32,
                                    P, P, SZ, P, P]
         L.moe_combine.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P, P]
+        L.moe_dispatch_ex.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, P,
+                                      I32, P, P, SZ, P, I32, P, I32, P]
+        L.moe_combine_ex.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P,
+                                     I32, P, I32, P]
         L.moe_expert_scale.argtypes = [P, P, I32, I32, I32, I32, I32, I32, P, P, P, P, I64, P]
         for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_dispatch",
-                  "moe_combine", "moe_expert_scale"):
+                  "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale"):
             getattr(L, f).restype = I32
         _lib = L
     return _lib
@@ -103,6 +114,12 @@ def moe_version() -> int:
     return lib().moe_version()
 
 
+def moe_wall_clock_khz() -> int:
+    out = I32(0)
+    _check("moe_wall_clock_khz", lib().moe_wall_clock_khz(ctypes.byref(out)))
+    return out.value
+
+
 def moe_layout_workspace_bytes(T: int, k: int, E: int, R: int) -> int:
     out = SZ(0)
     _check("moe_layout_workspace_bytes",
@@ -127,6 +144,28 @@ def moe_dispatch(x, x_scales, dtype, H, E, R, topk_idx, pos, rank_offset, recv_x
         _ptr(rank_offset), _ptr(recv_x), _ptr(recv_scales), scale_pitch, _ptr(recv_cap),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(status),
         _stream(stream)))
+
+
+def moe_dispatch_ex(x, x_scales, dtype, H, E, R, topk_idx, pos, rank_offset, row_src,
+                    recv_x, recv_scales, recv_cap, workspace, status, policy=MOE_POLICY_BALANCED,
+                    trace=None, stream=None, scale_pitch=0):
+    T, k = topk_idx.shape
+    _check("moe_dispatch_ex", lib().moe_dispatch_ex(
+        _ptr(x), _ptr(x_scales), dtype, T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
+        _ptr(rank_offset), _ptr(row_src), _ptr(recv_x), _ptr(recv_scales), scale_pitch,
+        _ptr(recv_cap), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(status), policy, _ptr(trace), 0 if trace is None else trace.numel() // 2,
+        _stream(stream)))
+
+
+def moe_combine_ex(expert_y, topk_w, H, E, R, topk_idx, pos, rank_offset, recv_cap, y,
+                   workspace, status, policy=MOE_POLICY_BALANCED, trace=None, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_combine_ex", lib().moe_combine_ex(
+        _ptr(expert_y), _ptr(topk_w), T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
+        _ptr(rank_offset), _ptr(recv_cap), _ptr(y), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(status), policy, _ptr(trace),
+        0 if trace is None else trace.numel() // 2, _stream(stream)))
 
 
 def moe_combine(expert_y, topk_w, H, E, R, topk_idx, pos, rank_offset, recv_cap, y,

@@ -40,7 +40,8 @@ class GpuRun:
     """One pass of layout -> dispatch -> expert -> combine on the GPU."""
 
     def __init__(self, cfg, inp, topk_idx=None, topk_w=None, spare_rows=0,
-                 cap_delta=None, identity=None, combine_on_dispatch=False, scale_pitch=None):
+                 cap_delta=None, identity=None, combine_on_dispatch=False, scale_pitch=None,
+                 policy=0, trace=False, combine_policy=0, repeat=1):
         self.cfg = cfg
         T, H, E, R = cfg["T"], cfg["H"], cfg["E"], cfg["R"]
         idx = inp["topk_idx"] if topk_idx is None else topk_idx
@@ -75,9 +76,15 @@ class GpuRun:
             self.sregions = moe.Regions(rows, self.scale_pitch, guard_bytes=GUARD,
                                         fill=SENTINEL)
             xs_d = to_dev(inp["x_scales"]).view(torch.float32)
-        moe.moe_dispatch(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
-                         self.regions.table, self.sregions.table if fp8 else None,
-                         cap_d, lay.workspace, lay.status, scale_pitch=self.scale_pitch)
+        self.dtrace = torch.zeros(2 * moe.MOE_PLAN_PARTS, dtype=torch.int64,
+                                  device="cuda") if trace else None
+        self.ctrace = torch.zeros_like(self.dtrace) if trace else None
+        for _ in range(repeat):   # repeats reuse one layout (and its work tickets)
+            moe.moe_dispatch_ex(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                                lay.row_src, self.regions.table,
+                                self.sregions.table if fp8 else None, cap_d, lay.workspace,
+                                lay.status, policy=policy, trace=self.dtrace,
+                                scale_pitch=self.scale_pitch)
 
         y = torch.empty((max(1, T), H), dtype=torch.int16, device="cuda")
         y.fill_(0x5A5A)
@@ -93,8 +100,10 @@ class GpuRun:
                                  self.eregions.table, max(1, T * k),
                                  scale_pitch=self.scale_pitch)
             ey_table = self.eregions.table
-        moe.moe_combine(ey_table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, cap_d,
-                        y, lay.workspace, lay.status)
+        for _ in range(repeat):
+            moe.moe_combine_ex(ey_table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, cap_d,
+                               y, lay.workspace, lay.status, policy=combine_policy,
+                               trace=self.ctrace)
         torch.cuda.synchronize()
 
         self.layout = dict(

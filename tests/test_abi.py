@@ -1,0 +1,135 @@
+"""The C ABI without a GPU: exported symbols and host-side argument checks.
+
+Every call here is rejected by validation before anything touches the GPU,
+so the tests run on the CPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_26444_amd import moe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(moe_\w+)\s*\(", text,
+                                 flags=re.M)))
+
+
+def test_header_declares_the_operator():
+    names = declared_functions()
+    for f in ("moe_layout", "moe_dispatch", "moe_combine", "moe_layout_workspace_bytes"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = moe.lib()
+    missing = [f for f in declared_functions() if not hasattr(lib, f)]
+    assert not missing, missing
+
+
+def test_binding_covers_every_declared_symbol():
+    assert sorted(moe.EXPORTS) == declared_functions()
+
+
+def test_version_and_strerror():
+    assert moe.moe_version() == 2
+    for code in (0, -1, -2, -3, -4, -99):
+        assert isinstance(moe.lib().moe_strerror(code), bytes)
+
+
+@pytest.mark.parametrize("T,k,E,R,code", [
+    (-1, 8, 256, 64, moe.MOE_EINVAL),       # negative tokens
+    (16, 0, 256, 64, moe.MOE_EINVAL),       # k < 1
+    (16, 33, 256, 64, moe.MOE_EINVAL),      # k > MOE_MAX_K
+    (16, 8, 4, 2, moe.MOE_EINVAL),          # k > E
+    (16, 8, 256, 60, moe.MOE_EINVAL),       # E % R != 0
+    (16, 8, 2048, 64, moe.MOE_EINVAL),      # E > MOE_MAX_EXPERTS
+    (2 ** 30, 8, 256, 64, moe.MOE_EINVAL),  # T*k beyond int32
+])
+def test_workspace_query_rejects_bad_shapes(T, k, E, R, code):
+    out = ctypes.c_size_t(0)
+    assert moe.lib().moe_layout_workspace_bytes(T, k, E, R, ctypes.byref(out)) == code
+
+
+def test_workspace_size_covers_plan_and_counts():
+    assert moe.moe_layout_workspace_bytes(16384, 8, 256, 64) >= (moe.MOE_PLAN_PARTS + 1) * 4
+    assert moe.moe_layout_workspace_bytes(0, 8, 256, 64) >= (moe.MOE_PLAN_PARTS + 1) * 4
+    assert moe.lib().moe_layout_workspace_bytes(16, 8, 256, 64, None) == moe.MOE_EINVAL
+
+
+FAKE = ctypes.c_void_p(0x10000)      # never dereferenced: calls fail validation
+MIS = ctypes.c_void_p(0x10008)       # 8-byte aligned, not 16
+WS = ctypes.c_void_p(0x100000)       # 256-byte aligned "workspace"
+
+
+def test_layout_argument_errors():
+    L = moe.lib()
+    n = moe.moe_layout_workspace_bytes(64, 8, 256, 64)
+    ok = [FAKE, 64, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, WS, n, FAKE, None]
+    bad = list(ok); bad[5] = None                      # null expert_count
+    assert L.moe_layout(*bad) == moe.MOE_EINVAL
+    bad = list(ok); bad[11] = ctypes.c_void_p(0x100010)  # misaligned workspace
+    assert L.moe_layout(*bad) == moe.MOE_EWORKSPACE
+    bad = list(ok); bad[12] = n - 4                    # workspace too small
+    assert L.moe_layout(*bad) == moe.MOE_EWORKSPACE
+    bad = list(ok); bad[4] = 48                        # E % R
+    assert L.moe_layout(*bad) == moe.MOE_EINVAL
+
+
+def _dispatch_args(**kw):
+    n = moe.moe_layout_workspace_bytes(64, 8, 256, 64)
+    a = dict(x=FAKE, xs=None, dtype=0, T=64, H=7168, k=8, E=256, R=64, idx=FAKE, pos=FAKE,
+             ro=FAKE, rs=FAKE, rx=FAKE, rsc=None, pitch=0, cap=FAKE, ws=WS, wsb=n,
+             st=FAKE, policy=0, trace=None, tw=0, stream=None)
+    a.update(kw)
+    return list(a.values())
+
+
+def test_dispatch_argument_errors():
+    L = moe.lib()
+    assert L.moe_dispatch_ex(*_dispatch_args(dtype=7)) == moe.MOE_EINVAL
+    assert L.moe_dispatch_ex(*_dispatch_args(policy=4)) == moe.MOE_EINVAL
+    assert L.moe_dispatch_ex(*_dispatch_args(policy=1, rs=None)) == moe.MOE_EINVAL
+    assert L.moe_dispatch_ex(*_dispatch_args(x=MIS)) == moe.MOE_EALIGN
+    assert L.moe_dispatch_ex(*_dispatch_args(H=7164)) == moe.MOE_EALIGN      # 2H % 16
+    assert L.moe_dispatch_ex(*_dispatch_args(dtype=1, xs=FAKE, rsc=FAKE,
+                                             H=7168 + 64)) == moe.MOE_EALIGN  # H % 128
+    assert L.moe_dispatch_ex(*_dispatch_args(dtype=1, xs=None, rsc=FAKE)) == moe.MOE_EINVAL
+    assert L.moe_dispatch_ex(*_dispatch_args(dtype=1, xs=FAKE, rsc=FAKE,
+                                             pitch=64)) == moe.MOE_EINVAL     # < 224 B
+    assert L.moe_dispatch_ex(*_dispatch_args(dtype=1, xs=FAKE, rsc=FAKE,
+                                             pitch=226)) == moe.MOE_EALIGN
+    assert L.moe_dispatch_ex(*_dispatch_args(wsb=16)) == moe.MOE_EWORKSPACE
+    assert L.moe_dispatch_ex(*_dispatch_args(rx=None)) == moe.MOE_EINVAL
+    assert L.moe_dispatch_ex(*_dispatch_args(trace=FAKE, tw=-1)) == moe.MOE_EINVAL
+
+
+def test_combine_argument_errors():
+    L = moe.lib()
+    n = moe.moe_layout_workspace_bytes(64, 8, 256, 64)
+    ok = [FAKE, FAKE, 64, 7168, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, WS, n, FAKE, 0, None,
+          0, None]
+    bad = list(ok); bad[11] = MIS                      # y misaligned
+    assert L.moe_combine_ex(*bad) == moe.MOE_EALIGN
+    bad = list(ok); bad[0] = None                      # null expert table
+    assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
+    bad = list(ok); bad[13] = 8
+    assert L.moe_combine_ex(*bad) == moe.MOE_EWORKSPACE
+    bad = list(ok); bad[4] = 300                       # k > MOE_MAX_K
+    assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
+    bad = list(ok); bad[15] = moe.MOE_POLICY_ROWS      # pull splits are dispatch-only
+    assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
+
+
+def test_no_fallback_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(moe, "_lib", None)
+    monkeypatch.setattr(moe, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="no fallback"):
+        moe.lib()

@@ -29,13 +29,15 @@ def _h():
 
 
 def _full_parity(cfg, inp=None, idx=None, w=None, spare_rows=2, cap_delta=None,
-                 identity=None, scale_pitch=None):
+                 identity=None, scale_pitch=None, policy=0, trace=False, combine_policy=0,
+                 repeat=1):
     h = _h()
     inp = wl.make_inputs(cfg) if inp is None else inp
     h.log(f"[parity] {cfg['name']} T={cfg['T']} H={cfg['H']} E={cfg['E']} R={cfg['R']} "
           f"k={(idx if idx is not None else inp['topk_idx']).shape[1]}")
     run = h.GpuRun(cfg, inp, topk_idx=idx, topk_w=w, spare_rows=spare_rows,
-                   cap_delta=cap_delta, identity=identity, scale_pitch=scale_pitch)
+                   cap_delta=cap_delta, identity=identity, scale_pitch=scale_pitch,
+                   policy=policy, trace=trace, combine_policy=combine_policy, repeat=repeat)
     ref = h.oracle_chain(cfg, inp, topk_idx=idx, topk_w=w, caps=run.caps,
                          identity=identity, scale_pitch=run.scale_pitch)
     # layout: bit-exact
@@ -126,6 +128,53 @@ def test_fp8_scale_pitch_too_small_is_rejected():
     with pytest.raises(moe.MoeError) as ei:
         h.GpuRun(cfg, wl.make_inputs(cfg), scale_pitch=64)
     assert ei.value.code == moe.MOE_EINVAL
+
+
+@pytest.mark.parametrize("policy", [1, 2])
+@pytest.mark.parametrize("T,H,E,R,k,payload,mask", [
+    (1000, 1032, 24, 6, 3, wl.BF16, 0.1),
+    (700, 640, 32, 8, 5, wl.FP8_E4M3, 0.05),
+    (2049, 7168, 256, 64, 8, wl.BF16, 0.0),
+    (513, 4096, 128, 32, 8, wl.FP8_E4M3, 0.0),
+])
+def test_pull_policies_match_oracle(policy, T, H, E, R, k, payload, mask):
+    """The pull work splits (rows even, or a fixed wavefront group per rank)
+    give the same bytes as the oracle, with a capacity overflow on one rank."""
+    cfg = wl.custom(T, H, E, R, k, payload=payload, seed=T + 1)
+    inp = wl.make_inputs(cfg)
+    idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
+    delta = [0] * R
+    delta[1] = -3
+    run, _ = _full_parity(cfg, inp, idx=idx, policy=policy, cap_delta=delta, spare_rows=1)
+
+
+@pytest.mark.parametrize("T,H,E,R,k,payload,mask", [
+    (1000, 1032, 24, 6, 3, wl.BF16, 0.1),
+    (700, 640, 32, 8, 5, wl.FP8_E4M3, 0.05),
+    (3000, 7168, 256, 64, 8, wl.BF16, 0.0),
+    (100, 256, 16, 4, 2, wl.BF16, 0.0),
+])
+def test_dynamic_policy_matches_oracle(T, H, E, R, k, payload, mask):
+    """Parts handed out at run time: same bytes for dispatch, same y for
+    combine; three calls on one layout exercise the ticket reset."""
+    cfg = wl.custom(T, H, E, R, k, payload=payload, zipf_s=1.2, seed=T + 2)
+    inp = wl.make_inputs(cfg)
+    idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
+    _full_parity(cfg, inp, idx=idx, policy=3, combine_policy=3, repeat=3)
+
+
+def test_trace_records_every_wavefront():
+    h = _h()
+    cfg = wl.custom(3000, 7168, 256, 64, 8, zipf_s=1.2, seed=5)
+    run = h.GpuRun(cfg, wl.make_inputs(cfg), trace=True)
+    for tr in (run.dtrace, run.ctrace):
+        t = tr.view(-1, 2).cpu().numpy()
+        used = t[:, 0] != 0
+        assert used.sum() >= 1024          # one record per launched wavefront
+        assert np.all(t[used, 1] >= t[used, 0])
+        assert np.all(t[~used] == 0)
+        span = t[used, 1].max() - t[used, 0].min()
+        assert 0 < span < 10 ** 9
 
 
 def test_all_slots_unused():
