@@ -136,6 +136,31 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
                size_t workspace_bytes, uint32_t* status, void* stream);
 
 /*
+ * moe_layout_fixed -- token placement into fixed-capacity expert windows:
+ * the low-latency form of the operator (Table 2's LL rows; the paper does
+ * not define the mode, this is the reading taken).  Expert e owns global rows
+ * [e*capacity, (e+1)*capacity), so every offset is known before routing and
+ * receive regions of L*capacity rows per rank can be allocated once; no host
+ * read of the counts is needed between layout and dispatch, and the whole
+ * layout -> dispatch -> combine chain can run inside one captured graph.
+ * Within a window rows are in token order; a routed slot whose rank within
+ * its expert reaches `capacity` is dropped (pos = -1, MOE_STATUS_CAPACITY).
+ *
+ * Out: expert_count[E] = rows placed per expert (<= capacity);
+ *      expert_offset[e] = e*capacity (E+1 entries);
+ *      rank_count[R] = rows placed per rank; rank_offset[r] = r*L*capacity;
+ *      pos[T*k] as moe_layout; row_src[E*capacity]: slot of each window row,
+ *      -1 for rows no slot fills; the partition plan counts placed slots.
+ * Dispatch and combine take these outputs unchanged (recv_cap[r] = L*capacity
+ * for regions sized to whole windows).  Errors as moe_layout, plus
+ * MOE_EINVAL for capacity < 0 or E*capacity > INT32_MAX.
+ */
+int moe_layout_fixed(const int32_t* topk_idx, int64_t T, int k, int E, int R, int capacity,
+                     int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
+                     int32_t* rank_offset, int32_t* pos, int32_t* row_src, void* workspace,
+                     size_t workspace_bytes, uint32_t* status, void* stream);
+
+/*
  * moe_dispatch -- copy every routed token row to its destination rank's
  * receive region (Section 6.1 remote-slice transfers with op = store, one
  * per routed slot; work split over wavefronts by bytes, Section 6.2 and

@@ -44,13 +44,15 @@ def lib():
         L.oracle_fp8e4m3_to_float.restype = ctypes.c_float
         L.oracle_layout.argtypes = [P_, I64, I32, I32, I32, P_, P_, P_, P_, P_, P_, P_]
         L.oracle_plan.argtypes = [P_, I64, I32, I32, P_]
+        L.oracle_layout_fixed.argtypes = [P_, I64, I32, I32, I32, I32, P_, P_, P_, P_, P_,
+                                          P_, P_]
         L.oracle_dispatch.argtypes = [P_, I64, P_, I64, I64, I64, I32, I32, I32, P_, P_,
                                       P_, P_, P_, P_, P_]
         L.oracle_expert_scale.argtypes = [P_, P_, I64, I32, I32, I32, I32, I32, P_, P_,
                                           P_, P_]
         L.oracle_combine.argtypes = [P_, P_, I64, I32, I32, I32, I32, P_, P_, P_,
                                      P_, P_, P_]
-        for f in ("oracle_layout", "oracle_plan", "oracle_dispatch",
+        for f in ("oracle_layout", "oracle_layout_fixed", "oracle_plan", "oracle_dispatch",
                   "oracle_expert_scale", "oracle_combine"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -101,6 +103,25 @@ def layout(topk_idx: np.ndarray, E: int, R: int) -> dict:
                              _p(out["rank_offset"]), _p(out["pos"]),
                              _p(out["row_src"]), _p(st))
     _check(rc, "oracle_layout")
+    out["status"] = int(st[0])
+    return out
+
+
+def layout_fixed(topk_idx: np.ndarray, E: int, R: int, C: int) -> dict:
+    """Fixed-capacity placement: expert windows of C rows (row_src has E*C)."""
+    idx = np.ascontiguousarray(topk_idx, dtype=np.int32)
+    T, k = idx.shape
+    out = dict(
+        expert_count=np.zeros(E, np.int32), expert_offset=np.zeros(E + 1, np.int32),
+        rank_count=np.zeros(R, np.int32), rank_offset=np.zeros(R + 1, np.int32),
+        pos=np.zeros(T * k, np.int32), row_src=np.zeros(max(1, E * C), np.int32))
+    st = np.zeros(1, np.uint32)
+    rc = lib().oracle_layout_fixed(_p(idx), T, k, E, R, C, _p(out["expert_count"]),
+                                   _p(out["expert_offset"]), _p(out["rank_count"]),
+                                   _p(out["rank_offset"]), _p(out["pos"]),
+                                   _p(out["row_src"]), _p(st))
+    _check(rc, "oracle_layout_fixed")
+    out["row_src"] = out["row_src"][: E * C]
     out["status"] = int(st[0])
     return out
 

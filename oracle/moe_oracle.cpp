@@ -154,6 +154,55 @@ int oracle_layout(const int32_t* topk_idx, int64_t T, int32_t k, int32_t E,
 }
 
 // ---------------------------------------------------------------------------
+// Fixed-capacity placement (the low-latency form of the operator, Table 2's
+// LL rows; the paper does not define the mode, this is the reading taken):
+// every expert owns a window of C rows, expert e's window starting at e*C,
+// so offsets are known without counting and receive regions (L*C rows per
+// rank) can be sized before routing is known.  Within a window rows are in
+// token order; a routed slot whose rank within its expert reaches C is
+// dropped (pos = -1, status bit 4).  expert_count / rank_count count placed
+// rows; expert_offset[e] = e*C, rank_offset[r] = r*L*C; row_src has E*C
+// entries, -1 for rows no slot fills.
+// ---------------------------------------------------------------------------
+int oracle_layout_fixed(const int32_t* topk_idx, int64_t T, int32_t k, int32_t E, int32_t R,
+                        int32_t C, int32_t* expert_count, int32_t* expert_offset,
+                        int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
+                        int32_t* row_src, uint32_t* status) {
+  if (T < 0 || k < 1 || E < 1 || R < 1 || E % R != 0 || C < 0) return -1;
+  const int32_t L = E / R;
+  uint32_t st = 0;
+  for (int32_t e = 0; e < E; ++e) expert_count[e] = 0;
+  for (int64_t i = 0; i < (int64_t)E * C; ++i) row_src[i] = -1;
+  for (int64_t t = 0; t < T; ++t) {
+    for (int32_t j = 0; j < k; ++j) {
+      const int64_t s = t * k + j;
+      const int32_t e = topk_idx[s];
+      pos[s] = -1;
+      if (e == -1) continue;
+      if (e < -1 || e >= E) { st |= kBadIndex; continue; }
+      bool repeat = false;
+      for (int32_t jj = 0; jj < j; ++jj)
+        if (topk_idx[t * k + jj] == e) repeat = true;
+      if (repeat) { st |= kDupIndex; continue; }
+      if (expert_count[e] >= C) { st |= kCapacity; continue; }
+      const int32_t p = e * C + expert_count[e];
+      expert_count[e] += 1;
+      pos[s] = p;
+      row_src[p] = (int32_t)s;
+    }
+  }
+  for (int32_t e = 0; e <= E; ++e) expert_offset[e] = e * C;
+  for (int32_t r = 0; r < R; ++r) {
+    rank_count[r] = 0;
+    for (int32_t e = r * L; e < (r + 1) * L; ++e) rank_count[r] += expert_count[e];
+    rank_offset[r] = r * L * C;
+  }
+  rank_offset[R] = E * C;
+  *status |= st;
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
 // Byte-balanced partition of the token range over P parts (Section 6.2 with a
 // single memory tier: every unit has the same cost model, the fan-out cap
 // does not bind, and a balanced split of the payload is what the list

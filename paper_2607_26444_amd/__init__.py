@@ -7,5 +7,5 @@ from .moe import (  # noqa: F401
     EXPORTS, MOE_DTYPE_BF16, MOE_DTYPE_FP8_E4M3, MOE_PLAN_PARTS, MOE_POLICY_BALANCED,
     MOE_POLICY_BY_RANK, MOE_POLICY_DYNAMIC, MOE_POLICY_ROWS, MOE_STATUS_BAD_INDEX, MOE_STATUS_CAPACITY,
     MOE_STATUS_DUP_INDEX, Layout, MoeError, Regions, lib, moe_combine, moe_combine_ex,
-    moe_dispatch, moe_dispatch_ex, moe_expert_scale, moe_layout, moe_layout_workspace_bytes,
+    moe_dispatch, moe_dispatch_ex, moe_expert_scale, moe_layout, moe_layout_fixed, moe_layout_workspace_bytes,
     moe_version)

@@ -104,9 +104,27 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R, int32_t*
   if (T > 0 && (!topk_idx || !pos || !row_src)) return MOE_EINVAL;
   if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
     return MOE_EWORKSPACE;
-  return launched(moe::launch_layout(topk_idx, T, k, E, R, expert_count, expert_offset,
+  return launched(moe::launch_layout(topk_idx, T, k, E, R, -1, expert_count, expert_offset,
                                      rank_count, rank_offset, pos, row_src, workspace, status,
                                      as_stream(stream)));
+}
+
+int moe_layout_fixed(const int32_t* topk_idx, int64_t T, int k, int E, int R, int capacity,
+                     int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
+                     int32_t* rank_offset, int32_t* pos, int32_t* row_src, void* workspace,
+                     size_t workspace_bytes, uint32_t* status, void* stream) {
+  int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  if (capacity < 0 || (int64_t)E * capacity > (int64_t)INT32_MAX) return MOE_EINVAL;
+  if (!expert_count || !expert_offset || !rank_count || !rank_offset || !workspace || !status)
+    return MOE_EINVAL;
+  if (T > 0 && (!topk_idx || !pos)) return MOE_EINVAL;
+  if (capacity > 0 && !row_src) return MOE_EINVAL;
+  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
+    return MOE_EWORKSPACE;
+  return launched(moe::launch_layout(topk_idx, T, k, E, R, capacity, expert_count,
+                                     expert_offset, rank_count, rank_offset, pos, row_src,
+                                     workspace, status, as_stream(stream)));
 }
 
 int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,

@@ -12,6 +12,9 @@
 //                 not serialize on a hot expert the way counter atomics do,
 //                 and the result does not depend on arrival order.
 //
+// A fixed-capacity variant places expert e's rows in the window
+// [e*C, (e+1)*C) instead of after the previous experts' rows.
+//
 //   layout_place  every chunk reads the whole count matrix (small by
 //                 construction, stored expert-major), derives the global
 //                 per-expert totals, their exclusive scan (expert_offset) and
@@ -130,9 +133,11 @@ constexpr int kMaxExpertsPerThread = MOE_MAX_EXPERTS / kBlock;  // 4
 // SINGLE: the whole batch is one sub-chunk (T <= kBlock), so this kernel
 // also does the counting (no layout_count launch): the totals are the
 // popcounts of its own bitmaps.
-template <int KW, bool SINGLE>
+// FIXED: fixed-capacity windows of C rows per expert (expert e's window
+// starts at e*C); a slot whose rank within its expert reaches C is dropped.
+template <int KW, bool SINGLE, bool FIXED>
 __global__ __launch_bounds__(kBlock) void layout_place_kernel(
-    const int32_t* __restrict__ idx, int64_t T, int k, int E, int R, int64_t chunk_tokens,
+    const int32_t* __restrict__ idx, int64_t T, int k, int E, int R, int C, int64_t chunk_tokens,
     int nc, int ncp, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
     int32_t* __restrict__ expert_offset, int32_t* __restrict__ rank_count,
     int32_t* __restrict__ rank_offset, int32_t* __restrict__ pos,
@@ -199,30 +204,35 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       }
     }
   }
+  // Rows each expert gets: all of its slots, or at most C in fixed windows.
   int64_t my_tot = 0, my_pre = 0;
 #pragma unroll
   for (int q = 0; q < kMaxExpertsPerThread; ++q) {
-    my_tot += tot[q];
-    my_pre += pre[q];
+    my_tot += FIXED ? min(tot[q], C) : tot[q];
+    my_pre += FIXED ? min(pre[q], C) : pre[q];
   }
   // One scan for both sums: totals in the high 32 bits, this chunk's prefix
   // in the low 32 (all sums are below 2^31, so no carry crosses).
   int64_t packed_total = 0;
   const int64_t packed = block_exclusive_scan((my_tot << 32) | my_pre, scan, packed_total);
   int64_t run = packed >> 32;                      // rows before my experts
-  const int64_t n_total = packed_total >> 32;       // routed slots N
-  const int64_t pre_total = packed_total & 0xFFFFFFFFll;  // routed slots before chunk
+  const int64_t n_total = packed_total >> 32;       // placed rows N
+  const int64_t pre_total = packed_total & 0xFFFFFFFFll;  // placed rows before chunk
+  // base[e]: window start of expert e (prefix sum, or e*C) plus its rows in
+  // earlier chunks; in fixed windows `base - e*C` is the rank within e.
+  // eoff[e]: rows placed before expert e (its packed offset), for rank_count.
 #pragma unroll
   for (int q = 0; q < kMaxExpertsPerThread; ++q) {
     const int e = tid * ept + q;
     if (q < ept && e < E) {
+      const int placed = FIXED ? min(tot[q], C) : tot[q];
       eoff[e] = (int32_t)run;
-      base[e] = (int32_t)(run + pre[q]);
+      base[e] = FIXED ? e * C + pre[q] : (int32_t)(run + pre[q]);
       if (c == 0) {
-        expert_count[e] = tot[q];
-        expert_offset[e] = (int32_t)run;
+        expert_count[e] = placed;
+        expert_offset[e] = FIXED ? e * C : (int32_t)run;
       }
-      run += tot[q];
+      run += placed;
     }
   }
   if (tid == 0) eoff[E] = (int32_t)n_total;
@@ -230,13 +240,13 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   if (c == 0) {
     const int L = E / R;
     if (tid == 0) {
-      expert_offset[E] = (int32_t)n_total;
-      rank_offset[R] = (int32_t)n_total;
+      expert_offset[E] = FIXED ? E * C : (int32_t)n_total;
+      rank_offset[R] = FIXED ? E * C : (int32_t)n_total;
       bound[0] = 0;
     }
     if (tid < 4) tickets[tid] = 0u;  // work tickets of dispatch and combine
     for (int r = tid; r < R; r += kBlock) {
-      rank_offset[r] = eoff[r * L];
+      rank_offset[r] = FIXED ? r * L * C : eoff[r * L];
       rank_count[r] = eoff[(r + 1) * L] - eoff[r * L];
     }
     if (T == 0)
@@ -261,9 +271,6 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       uint32_t st_more = 0;
       load_row<KW>(idx, t, c1, k, E, ev, ok, st_more);
     }
-    int nvalid = 0;
-#pragma unroll
-    for (int j = 0; j < KW; ++j) nvalid += ok[j] ? 1 : 0;
     if (!SINGLE) {
 #pragma unroll
       for (int j = 0; j < KW; ++j)
@@ -271,6 +278,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       __syncthreads();
     }
     const uint64_t below = (1ull << lane) - 1ull;
+    int nplaced = 0;
 #pragma unroll
     for (int j = 0; j < KW; ++j) {
       if (t < c1 && j < k) {
@@ -279,15 +287,20 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
           const int e = ev[j];
           int r = base[e] + __popcll(mask[w * E + e] & below);
           for (int q = 0; q < w; ++q) r += __popcll(mask[q * E + e]);
-          p = r;
-          row_src[p] = (int32_t)(t * k + j);
+          if (!FIXED || r - e * C < C) {
+            p = r;
+            row_src[p] = (int32_t)(t * k + j);
+            ++nplaced;
+          } else {
+            st |= MOE_STATUS_CAPACITY;
+          }
         }
         pos[t * k + j] = p;
       }
     }
     // Plan boundaries inside this sub-chunk: token t owns the parts p with
     // a_t*P < p*A <= (a_t + cost_t)*P, each starting at token t+1.
-    const int64_t cost = (t < c1) ? 1 + nvalid : 0;
+    const int64_t cost = (t < c1) ? 1 + nplaced : 0;
     int64_t sub_total = 0;
     const int64_t a = cost_base + block_exclusive_scan(cost, scan, sub_total);
     if (cost) {
@@ -308,17 +321,24 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     __syncthreads();
   }
 
-  // Rows past the last routed slot have no source.
-  for (int64_t i = n_total + (int64_t)c * kBlock + tid; i < T * k; i += (int64_t)nc * kBlock)
-    row_src[i] = -1;
-  if (SINGLE) {
-    st = wave_or(st);
-    if (lane == 0 && st) atomicOr(status, st);
+  if (FIXED) {
+    // Window rows no slot fills have no source: for the experts this chunk
+    // owns (e = c, c + nc, ...), rows [e*C + placed_e, (e+1)*C).
+    for (int e = c; e < E; e += nc) {
+      const int placed = eoff[e + 1] - eoff[e];
+      for (int i = placed + tid; i < C; i += kBlock) row_src[(int64_t)e * C + i] = -1;
+    }
+  } else {
+    // Rows past the last routed slot have no source.
+    for (int64_t i = n_total + (int64_t)c * kBlock + tid; i < T * k; i += (int64_t)nc * kBlock)
+      row_src[i] = -1;
   }
+  st = wave_or(st);
+  if (lane == 0 && st) atomicOr(status, st);
 }
 
-template <int KW>
-hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
+template <int KW, bool FIXED>
+hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R, int C,
                             int32_t* expert_count, int32_t* expert_offset,
                             int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
                             int32_t* row_src, void* workspace, uint32_t* status,
@@ -331,8 +351,9 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
   const size_t lds_place = (size_t)kWavesPerBlock * E * 8 + kWavesPerBlock * 8 +
                            (size_t)E * 4 + (size_t)(E + 1) * 4;
   if (g.nc == 1 && T <= kBlock) {
-    hipLaunchKernelGGL((layout_place_kernel<KW, true>), dim3(1), dim3(kBlock), lds_place, stream,
-                       idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
+    hipLaunchKernelGGL((layout_place_kernel<KW, true, FIXED>), dim3(1), dim3(kBlock), lds_place,
+                       stream, idx, T, k, E, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
+                       expert_count,
                        expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
                        status);
     return hipGetLastError();
@@ -341,8 +362,9 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R,
                      idx, T, k, E, g.chunk_tokens, g.ncp, counts, status);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((layout_place_kernel<KW, false>), dim3(g.nc), dim3(kBlock), lds_place,
-                     stream, idx, T, k, E, R, g.chunk_tokens, g.nc, g.ncp, counts, expert_count,
+  hipLaunchKernelGGL((layout_place_kernel<KW, false, FIXED>), dim3(g.nc), dim3(kBlock),
+                     lds_place, stream, idx, T, k, E, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
+                     expert_count,
                      expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
                      status);
   return hipGetLastError();
@@ -373,28 +395,45 @@ int slot_width(int k) {
   return kw;
 }
 
-hipError_t launch_layout(const int32_t* idx, int64_t T, int k, int E, int R,
-                         int32_t* expert_count, int32_t* expert_offset,
-                         int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
-                         int32_t* row_src, void* workspace, uint32_t* status,
-                         hipStream_t stream) {
+template <bool FIXED>
+hipError_t launch_layout_fx(const int32_t* idx, int64_t T, int k, int E, int R, int C,
+                            int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
+                            int32_t* rank_offset, int32_t* pos, int32_t* row_src,
+                            void* workspace, uint32_t* status, hipStream_t stream) {
   switch (slot_width(k)) {
     case 2:
-      return launch_layout_kw<2>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
-                                 rank_offset, pos, row_src, workspace, status, stream);
+      return launch_layout_kw<2, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+                                        rank_count, rank_offset, pos, row_src, workspace,
+                                        status, stream);
     case 4:
-      return launch_layout_kw<4>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
-                                 rank_offset, pos, row_src, workspace, status, stream);
+      return launch_layout_kw<4, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+                                        rank_count, rank_offset, pos, row_src, workspace,
+                                        status, stream);
     case 8:
-      return launch_layout_kw<8>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
-                                 rank_offset, pos, row_src, workspace, status, stream);
+      return launch_layout_kw<8, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+                                        rank_count, rank_offset, pos, row_src, workspace,
+                                        status, stream);
     case 16:
-      return launch_layout_kw<16>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
-                                  rank_offset, pos, row_src, workspace, status, stream);
+      return launch_layout_kw<16, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+                                         rank_count, rank_offset, pos, row_src, workspace,
+                                         status, stream);
     default:
-      return launch_layout_kw<32>(idx, T, k, E, R, expert_count, expert_offset, rank_count,
-                                  rank_offset, pos, row_src, workspace, status, stream);
+      return launch_layout_kw<32, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+                                         rank_count, rank_offset, pos, row_src, workspace,
+                                         status, stream);
   }
+}
+
+hipError_t launch_layout(const int32_t* idx, int64_t T, int k, int E, int R, int fixed_cap,
+                         int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
+                         int32_t* rank_offset, int32_t* pos, int32_t* row_src, void* workspace,
+                         uint32_t* status, hipStream_t stream) {
+  if (fixed_cap >= 0)
+    return launch_layout_fx<true>(idx, T, k, E, R, fixed_cap, expert_count, expert_offset,
+                                  rank_count, rank_offset, pos, row_src, workspace, status,
+                                  stream);
+  return launch_layout_fx<false>(idx, T, k, E, R, 0, expert_count, expert_offset, rank_count,
+                                 rank_offset, pos, row_src, workspace, status, stream);
 }
 
 }  // namespace moe

@@ -45,8 +45,9 @@ int slot_width(int k);
 // of kWavesPerBlock.  Queried once per (device, kernel) and cached.
 int resident_waves(const void* kernel, size_t lds_bytes);
 
+// fixed_cap < 0: packed layout; >= 0: fixed windows of fixed_cap rows.
 hipError_t launch_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
-                         int32_t* expert_count, int32_t* expert_offset,
+                         int fixed_cap, int32_t* expert_count, int32_t* expert_offset,
                          int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
                          int32_t* row_src, void* workspace, uint32_t* status,
                          hipStream_t stream);

@@ -41,7 +41,7 @@ MOE_POLICY_DYNAMIC = 3
 
 # Entry points declared in include/moe.h.
 EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error", "moe_wall_clock_khz",
-           "moe_layout_workspace_bytes", "moe_layout", "moe_dispatch",
+           "moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
            "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale")
 
 _lib = None
@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
         L.moe_wall_clock_khz.restype = I32
         L.moe_layout_workspace_bytes.argtypes = [I64, I32, I32, I32, ctypes.POINTER(SZ)]
         L.moe_layout.argtypes = [P, I64, I32, I32, I32, P, P, P, P, P, P, P, SZ, P, P]
+        L.moe_layout_fixed.argtypes = [P, I64, I32, I32, I32, I32, P, P, P, P, P, P, P, SZ, P,
+                                       P]
         L.moe_dispatch.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, I32,
                                    P, P, SZ, P, P]
         L.moe_combine.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P, P]
@@ -85,7 +87,7 @@ def lib() -> ctypes.CDLL:
         L.moe_combine_ex.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P,
                                      I32, P, I32, P]
         L.moe_expert_scale.argtypes = [P, P, I32, I32, I32, I32, I32, I32, P, P, P, P, I64, P]
-        for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_dispatch",
+        for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
                   "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale"):
             getattr(L, f).restype = I32
         _lib = L
@@ -132,6 +134,15 @@ def moe_layout(topk_idx, E, R, expert_count, expert_offset, rank_count, rank_off
     T, k = topk_idx.shape
     _check("moe_layout", lib().moe_layout(
         _ptr(topk_idx), T, k, E, R, _ptr(expert_count), _ptr(expert_offset),
+        _ptr(rank_count), _ptr(rank_offset), _ptr(pos), _ptr(row_src), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(status), _stream(stream)))
+
+
+def moe_layout_fixed(topk_idx, E, R, capacity, expert_count, expert_offset, rank_count,
+                     rank_offset, pos, row_src, workspace, status, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_layout_fixed", lib().moe_layout_fixed(
+        _ptr(topk_idx), T, k, E, R, capacity, _ptr(expert_count), _ptr(expert_offset),
         _ptr(rank_count), _ptr(rank_offset), _ptr(pos), _ptr(row_src), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(status), _stream(stream)))
 
@@ -187,17 +198,19 @@ def moe_expert_scale(recv_x, recv_scales, dtype, H, E, R, identity, expert_offse
 
 # ------------------------------------------------------------ buffer plumbing
 class Layout:
-    """Device outputs of moe_layout for one batch shape."""
+    """Device outputs of moe_layout (capacity None) or moe_layout_fixed
+    (windows of `capacity` rows per expert) for one batch shape."""
 
-    def __init__(self, T, k, E, R, device="cuda"):
+    def __init__(self, T, k, E, R, device="cuda", capacity=None):
         i32 = dict(dtype=torch.int32, device=device)
-        self.T, self.k, self.E, self.R = T, k, E, R
+        self.T, self.k, self.E, self.R, self.capacity = T, k, E, R, capacity
         self.expert_count = torch.empty(E, **i32)
         self.expert_offset = torch.empty(E + 1, **i32)
         self.rank_count = torch.empty(R, **i32)
         self.rank_offset = torch.empty(R + 1, **i32)
         self.pos = torch.empty(max(1, T * k), **i32)
-        self.row_src = torch.empty(max(1, T * k), **i32)
+        rows = T * k if capacity is None else E * capacity
+        self.row_src = torch.empty(max(1, rows), **i32)
         nbytes = moe_layout_workspace_bytes(T, k, E, R)
         # torch's caching allocator returns 512-byte aligned blocks
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
@@ -205,9 +218,14 @@ class Layout:
         self.status = torch.zeros(1, dtype=torch.int32, device=device)
 
     def run(self, topk_idx, stream=None):
-        moe_layout(topk_idx, self.E, self.R, self.expert_count, self.expert_offset,
-                   self.rank_count, self.rank_offset, self.pos, self.row_src,
-                   self.workspace, self.status, stream)
+        if self.capacity is None:
+            moe_layout(topk_idx, self.E, self.R, self.expert_count, self.expert_offset,
+                       self.rank_count, self.rank_offset, self.pos, self.row_src,
+                       self.workspace, self.status, stream)
+        else:
+            moe_layout_fixed(topk_idx, self.E, self.R, self.capacity, self.expert_count,
+                             self.expert_offset, self.rank_count, self.rank_offset, self.pos,
+                             self.row_src, self.workspace, self.status, stream)
 
     def plan(self):
         """The partition plan bound[MOE_PLAN_PARTS + 1] (a view of the workspace)."""

@@ -41,7 +41,7 @@ class GpuRun:
 
     def __init__(self, cfg, inp, topk_idx=None, topk_w=None, spare_rows=0,
                  cap_delta=None, identity=None, combine_on_dispatch=False, scale_pitch=None,
-                 policy=0, trace=False, combine_policy=0, repeat=1):
+                 policy=0, trace=False, combine_policy=0, repeat=1, capacity=None):
         self.cfg = cfg
         T, H, E, R = cfg["T"], cfg["H"], cfg["E"], cfg["R"]
         idx = inp["topk_idx"] if topk_idx is None else topk_idx
@@ -54,11 +54,14 @@ class GpuRun:
 
         idx_d = to_dev(idx.astype(np.int32))
         w_d = to_dev(w.astype(np.float32))
-        lay = moe.Layout(T, k, E, R)
+        lay = moe.Layout(T, k, E, R, capacity=capacity)
         lay.run(idx_d)
         torch.cuda.synchronize()
         counts = lay.rank_count.cpu().numpy()
-        caps = counts.astype(np.int64) + spare_rows
+        if capacity is None:
+            caps = counts.astype(np.int64) + spare_rows
+        else:   # whole expert windows, no count needed
+            caps = np.full(R, (E // R) * capacity, np.int64)
         if cap_delta is not None:
             caps = np.maximum(0, caps + np.asarray(cap_delta))
         self.caps = caps.astype(np.int32)
@@ -97,7 +100,8 @@ class GpuRun:
             moe.moe_expert_scale(self.regions.table,
                                  self.sregions.table if fp8 else None, dtype, H, E, R,
                                  ident, lay.expert_offset, lay.rank_offset, cap_d,
-                                 self.eregions.table, max(1, T * k),
+                                 self.eregions.table,
+                                 max(1, T * k if capacity is None else E * capacity),
                                  scale_pitch=self.scale_pitch)
             ey_table = self.eregions.table
         for _ in range(repeat):
@@ -106,13 +110,14 @@ class GpuRun:
                                trace=self.ctrace)
         torch.cuda.synchronize()
 
+        nrows = T * k if capacity is None else E * capacity
         self.layout = dict(
             expert_count=lay.expert_count.cpu().numpy(),
             expert_offset=lay.expert_offset.cpu().numpy(),
             rank_count=counts,
             rank_offset=lay.rank_offset.cpu().numpy(),
             pos=lay.pos.cpu().numpy()[: T * k],
-            row_src=lay.row_src.cpu().numpy()[: T * k],
+            row_src=lay.row_src.cpu().numpy()[:nrows],
             status=int(lay.status.cpu().numpy()[0]))
         self.plan = lay.plan().cpu().numpy()
         self.y = y.cpu().numpy().view(np.uint16)[:T]
@@ -123,13 +128,14 @@ class GpuRun:
 
 
 def oracle_chain(cfg, inp, topk_idx=None, topk_w=None, caps=None, identity=None,
-                 combine_on_dispatch=False, scale_pitch=0):
+                 combine_on_dispatch=False, scale_pitch=0, capacity=None):
     E, R, H = cfg["E"], cfg["R"], cfg["H"]
     idx = inp["topk_idx"] if topk_idx is None else topk_idx
     w = inp["topk_w"] if topk_w is None else topk_w
     fp8 = cfg["payload"] == wl.FP8_E4M3
     ident = (cfg["expert"] == "identity") if identity is None else identity
-    lay = oracle.layout(idx, E, R)
+    lay = oracle.layout(idx, E, R) if capacity is None else \
+        oracle.layout_fixed(idx, E, R, capacity)
     cap = lay["rank_count"] if caps is None else caps
     xs = u8_rows(inp["x_scales"]) if fp8 else None
     regs, sregs, st_d = oracle.dispatch(u8_rows(inp["x"]), xs, idx, lay["pos"],

@@ -273,6 +273,70 @@ def pin_layout_slot_permutation_invariance():
     assert np.array_equal(a["row_src"] // k, b["row_src"] // k)
 
 
+def layout_fixed_bruteforce(idx, E, R, C):
+    """Fixed windows from the definition: a routed slot's rank within its
+    expert is the number of earlier tokens routed to the same expert; it is
+    placed at e*C + rank when rank < C."""
+    T, k = idx.shape
+    L = E // R
+    base = layout_bruteforce(idx, E, R)     # validity and status bits 1, 2
+    pos = -np.ones(T * k, np.int64)
+    st = base["status"]
+    count = np.zeros(E, np.int64)
+    for t in range(T):
+        for j in range(k):
+            if base["pos"][t * k + j] < 0:
+                continue
+            e = int(idx[t, j])
+            rank = sum(1 for tt in range(t) for jj in range(k)
+                       if base["pos"][tt * k + jj] >= 0 and idx[tt, jj] == e)
+            if rank < C:
+                pos[t * k + j] = e * C + rank
+                count[e] += 1
+            else:
+                st |= 4
+    row_src = -np.ones(E * C, np.int64)
+    for s_ in range(T * k):
+        if pos[s_] >= 0:
+            row_src[pos[s_]] = s_
+    return dict(expert_count=count, expert_offset=np.arange(E + 1) * C,
+                rank_count=count.reshape(R, L).sum(1), rank_offset=np.arange(R + 1) * L * C,
+                pos=pos, row_src=row_src, status=st)
+
+
+def pin_layout_fixed_bruteforce():
+    rng = np.random.Generator(np.random.PCG64(25))
+    for case in range(80):
+        E = int(rng.choice([4, 8, 16]))
+        R = int(rng.choice([r for r in (1, 2, 4) if E % r == 0]))
+        k = int(rng.integers(1, min(E, 4) + 1))
+        T = int(rng.integers(0, 20))
+        C = int(rng.integers(0, 8))
+        idx = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32) \
+            if T else np.zeros((0, k), np.int32)
+        if case % 3 == 0 and T:
+            idx[rng.random(idx.shape) < 0.2] = -1
+        if case % 5 == 0 and T:
+            idx[0, 0] = E + 1
+        _assert_layout_equal(oracle.layout_fixed(idx, E, R, C),
+                             layout_fixed_bruteforce(idx, E, R, C), case)
+
+
+def pin_layout_fixed_large_capacity_equals_packed():
+    """With C >= every expert's count, the fixed windows hold exactly the
+    packed layout's rows, each window shifted to e*C."""
+    idx, _ = wl.make_routing(wl.get("decode"))
+    E, R = 256, 64
+    packed = oracle.layout(idx, E, R)
+    C = int(packed["expert_count"].max())
+    fixed = oracle.layout_fixed(idx, E, R, C)
+    assert fixed["status"] == 0
+    assert np.array_equal(fixed["expert_count"], packed["expert_count"])
+    e = np.where(idx.ravel() >= 0, idx.ravel(), 0)
+    shift = e * C - packed["expert_offset"][e]
+    assert np.array_equal(fixed["pos"], packed["pos"] + shift)
+
+
 # ----------------------------------------------------------------- plan
 def _plan_bruteforce(pos, T, k, P):
     cost = [1 + sum(1 for j in range(k) if pos[t * k + j] >= 0) for t in range(T)]

@@ -30,16 +30,17 @@ def _h():
 
 def _full_parity(cfg, inp=None, idx=None, w=None, spare_rows=2, cap_delta=None,
                  identity=None, scale_pitch=None, policy=0, trace=False, combine_policy=0,
-                 repeat=1):
+                 repeat=1, capacity=None):
     h = _h()
     inp = wl.make_inputs(cfg) if inp is None else inp
     h.log(f"[parity] {cfg['name']} T={cfg['T']} H={cfg['H']} E={cfg['E']} R={cfg['R']} "
           f"k={(idx if idx is not None else inp['topk_idx']).shape[1]}")
     run = h.GpuRun(cfg, inp, topk_idx=idx, topk_w=w, spare_rows=spare_rows,
                    cap_delta=cap_delta, identity=identity, scale_pitch=scale_pitch,
-                   policy=policy, trace=trace, combine_policy=combine_policy, repeat=repeat)
+                   policy=policy, trace=trace, combine_policy=combine_policy, repeat=repeat,
+                   capacity=capacity)
     ref = h.oracle_chain(cfg, inp, topk_idx=idx, topk_w=w, caps=run.caps,
-                         identity=identity, scale_pitch=run.scale_pitch)
+                         identity=identity, scale_pitch=run.scale_pitch, capacity=capacity)
     # layout: bit-exact
     for key in ("expert_count", "expert_offset", "rank_count", "rank_offset", "pos",
                 "row_src"):
@@ -52,7 +53,8 @@ def _full_parity(cfg, inp=None, idx=None, w=None, spare_rows=2, cap_delta=None,
     if run.sregions is not None:
         h.check_regions(run, run.sregions, ref["sregs"])
     # stand-in expert: bit-exact
-    written = np.minimum(ref["layout"]["rank_count"], run.caps)
+    written = np.minimum(ref["layout"]["rank_count"], run.caps) if capacity is None \
+        else run.caps   # fixed windows: the stand-in expert runs over whole windows
     h.check_regions(run, run.eregions,
                     [e.view(np.uint8).reshape(e.shape[0], 2 * e.shape[1]) for e in ref["ey"]],
                     written)
@@ -161,6 +163,69 @@ def test_dynamic_policy_matches_oracle(T, H, E, R, k, payload, mask):
     inp = wl.make_inputs(cfg)
     idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
     _full_parity(cfg, inp, idx=idx, policy=3, combine_policy=3, repeat=3)
+
+
+@pytest.mark.parametrize("T,H,E,R,k,payload,C,zipf", [
+    (1000, 1032, 24, 6, 3, wl.BF16, 200, 0.0),      # ample windows
+    (1000, 1032, 24, 6, 3, wl.BF16, 60, 1.2),       # hot experts overflow
+    (700, 640, 32, 8, 5, wl.FP8_E4M3, 90, 1.2),
+    (4096, 7168, 256, 64, 8, wl.BF16, 160, 0.0),    # decode-sized share
+    (200, 256, 16, 4, 2, wl.BF16, 0, 0.0),          # zero capacity: nothing placed
+    (100, 512, 16, 4, 4, wl.BF16, 7, 0.0),          # single-kernel layout
+])
+def test_fixed_capacity_layout(T, H, E, R, k, payload, C, zipf):
+    cfg = wl.custom(T, H, E, R, k, payload=payload, zipf_s=zipf, seed=T + C)
+    inp = wl.make_inputs(cfg)
+    run, ref = _full_parity(cfg, inp, capacity=C)
+    overflow = (ref["layout"]["status"] & 4) != 0
+    assert overflow == bool((np.bincount(inp["topk_idx"].ravel(), minlength=E) > C).any())
+
+
+def test_fixed_capacity_step_in_a_captured_graph():
+    """layout_fixed -> dispatch -> combine captured once and replayed; each
+    replay (with eager work in between) matches the eager result."""
+    from paper_2607_26444_amd import moe
+    cfg = wl.custom(2048, 7168, 256, 64, 8, zipf_s=1.2, seed=9)
+    inp = wl.make_inputs(cfg)
+    T, H, E, R, k, C = 2048, 7168, 256, 64, 8, 256
+    L = E // R
+    dev = "cuda"
+    x_d = torch.from_numpy(np.ascontiguousarray(inp["x"]).view(np.int16)).to(dev)
+    idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
+    w_d = torch.from_numpy(inp["topk_w"]).to(dev)
+    lay = moe.Layout(T, k, E, R, capacity=C)
+    regions = moe.Regions([L * C] * R, 2 * H)
+    y = torch.zeros((T, H), dtype=torch.int16, device=dev)
+
+    def step():
+        lay.run(idx_d)
+        moe.moe_dispatch(x_d, None, 0, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                         regions.table, None, regions.cap, lay.workspace, lay.status)
+        moe.moe_combine(regions.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                        regions.cap, y, lay.workspace, lay.status)
+
+    step()
+    torch.cuda.synchronize()
+    eager = y.clone()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()          # warm the occupancy cache on this stream
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step()
+    for i in range(4):
+        y.fill_(0)
+        lay.pos.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager), i
+    # Zipf(1.2) sends ~2000 of the 16384 slots to the hottest expert, far
+    # above the 256-row windows: those slots are dropped and flagged
+    assert int(lay.status.item()) == moe.MOE_STATUS_CAPACITY
 
 
 def test_trace_records_every_wavefront():

@@ -41,6 +41,10 @@ MUTANTS = [
     ("layout_row_src_stores_token", "row_src[p] = (int32_t)s;", "row_src[p] = (int32_t)(s / k);"),
     ("layout_token_order_reversed", "for (int64_t t = 0; t < T; ++t) {\n    for (int32_t j = 0; j < k; ++j) {\n      int64_t s = t * k + j;",
      "for (int64_t t = T - 1; t >= 0; --t) {\n    for (int32_t j = 0; j < k; ++j) {\n      int64_t s = t * k + j;"),
+    ("fixed_keeps_overflow", "if (expert_count[e] >= C) { st |= kCapacity; continue; }",
+     "if (expert_count[e] >= C + 1) { st |= kCapacity; continue; }"),
+    ("fixed_window_reversed", "const int32_t p = e * C + expert_count[e];",
+     "const int32_t p = e * C + (C - 1 - expert_count[e]);"),
     ("plan_cost_ignores_read", "int64_t c = 1;", "int64_t c = 0;"),
     ("plan_boundary_off_by_one", "a[(size_t)t] * P < p * A", "a[(size_t)t] * P <= p * A"),
     ("dispatch_short_copy", "x + t * row_bytes, (size_t)row_bytes);",
