@@ -33,6 +33,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
 
 
+def _num(v, nd):
+    return None if v != v else round(v, nd)   # NaN -> null
+
+
 def algorithmic_bytes(cfg) -> dict:
     T, H, k = cfg["T"], cfg["H"], cfg["k"]
     fp8 = cfg["payload"] == 1
@@ -228,6 +232,10 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the step benchmark: dispatch under each work split")
+    ap.add_argument("--ll", type=float, default=None, metavar="F",
+                    help="fixed-capacity layout with windows of F x the mean expert load")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture each step in a graph (needs --ll: no host sync in a step)")
     a = ap.parse_args(argv)
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the operator; runs on more than "
@@ -256,11 +264,19 @@ def main(argv=None):
     idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
     w_d = torch.from_numpy(inp["topk_w"]).to(dev)
 
-    lay = moe.Layout(T, k, E, R)
+    if a.graph and a.ll is None:
+        print("--graph needs --ll (the packed layout reads counts back to size regions)",
+              file=sys.stderr)
+        return 2
+    capacity = None if a.ll is None else max(1, int(np.ceil(a.ll * T * k / E)))
+    lay = moe.Layout(T, k, E, R, capacity=capacity)
     lay.run(idx_d)
     torch.cuda.synchronize()
-    counts = lay.rank_count.cpu().numpy()
-    rows = [max(1, int(c)) for c in counts]
+    if capacity is None:
+        counts = lay.rank_count.cpu().numpy()
+        rows = [max(1, int(c)) for c in counts]
+    else:   # whole windows, sized before routing is known
+        rows = [(E // R) * capacity] * R
     rb, sb = wl.row_bytes(cfg), wl.scale_row_bytes(cfg)
     spitch = (sb + 127) // 128 * 128   # scale rows on whole 128-byte lines
     regions = moe.Regions(rows, rb)
@@ -281,7 +297,7 @@ def main(argv=None):
     dispatch()
     moe.moe_expert_scale(regions.table, sregions.table if fp8 else None, dtype, H, E, R,
                          cfg["expert"] == "identity", lay.expert_offset, lay.rank_offset,
-                         regions.cap, eregions.table, T * k, scale_pitch=spitch)
+                         regions.cap, eregions.table, sum(rows), scale_pitch=spitch)
     torch.cuda.synchronize()
 
     for _ in range(a.warmup):
@@ -292,22 +308,49 @@ def main(argv=None):
     status = int(lay.status.item())
     if status != 0:
         print(f"[bench] status word {status} after warmup", file=sys.stderr)
+        if capacity is not None and status == moe.MOE_STATUS_CAPACITY:
+            ti = inp["topk_idx"]
+            need = np.bincount(ti[ti >= 0].ravel(), minlength=E).max() * E / (T * k)
+            print(f"[bench] the fixed windows drop slots: the busiest expert needs "
+                  f"--ll {need:.2f} or more", file=sys.stderr)
         return 1
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
+    graph = None
+    if a.graph:
+        # one graph per step; events stay outside it (recorded around replays)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            lay.run(idx_d)
+            dispatch()
+            combine()
+        torch.cuda.synchronize()
+        for _ in range(3):
+            graph.replay()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
     print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(a.steps):
         ev[s][0].record(stream)
-        lay.run(idx_d)
-        ev[s][1].record(stream)
-        dispatch()
-        ev[s][2].record(stream)
-        combine()
+        if graph is not None:
+            graph.replay()
+            ev[s][1].record(stream)
+            ev[s][2].record(stream)
+        else:
+            lay.run(idx_d)
+            ev[s][1].record(stream)
+            dispatch()
+            ev[s][2].record(stream)
+            combine()
         ev[s][3].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    status = int(lay.status.item())
+    if status != 0:
+        print(f"[bench] status word {status} after timing", file=sys.stderr)
+        return 1
 
     lay_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
     dis_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
@@ -317,12 +360,18 @@ def main(argv=None):
     dc_bytes = b["dispatch"] + b["combine"]
     value = dc_bytes / (step_ms * 1e-3) / 1e9
     d_us, c_us, l_us = dis_ms.mean() * 1e3, com_ms.mean() * 1e3, lay_ms.mean() * 1e3
+    if graph is not None:
+        # a replayed graph has no per-kernel events: whole-step figures only
+        dom, dom_bytes, dom_us = "layout+dispatch+combine (graph)", dc_bytes, c_us
+        d_us = c_us = l_us = float("nan")
+        traffic = None
+    else:
+        dom = "dispatch" if d_us >= c_us else "combine"
+        dom_bytes, dom_us = (b["dispatch"], d_us) if dom == "dispatch" else (b["combine"], c_us)
+        traffic = read_traffic(cfg["name"], dom)
     d_gbps = b["dispatch"] / (d_us * 1e-6) / 1e9
     c_gbps = b["combine"] / (c_us * 1e-6) / 1e9
-    dom = "dispatch" if d_us >= c_us else "combine"
-    dom_bytes, dom_us = (b["dispatch"], d_us) if dom == "dispatch" else (b["combine"], c_us)
     achieved = dom_bytes / (dom_us * 1e-6) / 1e9
-    traffic = read_traffic(cfg["name"], dom)
 
     out = {
         "metric": "dispatch+combine effective GB/s (algorithmic bytes / whole-step time)",
@@ -339,15 +388,17 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": cfg["name"], "T": T, "H": H, "E": E, "R": R, "k": k,
                    "payload": "fp8_e4m3" if fp8 else "bf16", "zipf_s": cfg["zipf_s"],
-                   "force_frac": cfg["force_frac"], "parallelism": "1 GPU, R emulated ranks"},
+                   "force_frac": cfg["force_frac"], "parallelism": "1 GPU, R emulated ranks",
+                   "layout": "packed" if capacity is None else f"fixed windows of {capacity}",
+                   "graph": bool(graph is not None)},
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "tokens_per_s": round(T / (step_ms * 1e-3), 1),
-        "layout_us": round(l_us, 2),
-        "dispatch_us": round(d_us, 2),
-        "combine_us": round(c_us, 2),
-        "dispatch_GBps": round(d_gbps, 1),
-        "combine_GBps": round(c_gbps, 1),
-        "dispatch_plus_combine_GBps": round(dc_bytes / ((d_us + c_us) * 1e-6) / 1e9, 1),
+        "layout_us": _num(l_us, 2),
+        "dispatch_us": _num(d_us, 2),
+        "combine_us": _num(c_us, 2),
+        "dispatch_GBps": _num(d_gbps, 1),
+        "combine_GBps": _num(c_gbps, 1),
+        "dispatch_plus_combine_GBps": _num(dc_bytes / ((d_us + c_us) * 1e-6) / 1e9, 1),
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
