@@ -167,15 +167,14 @@ def ablation(a):
            "rank_rows_max_over_mean": round(max(rows) / (sum(rows) / len(rows)), 2),
            "wall_clock_khz": khz, "policies": {}}
     b = algorithmic_bytes(cfg)
-    for name, pol in (("balanced_push", moe.MOE_POLICY_BALANCED),
-                      ("dynamic_push", moe.MOE_POLICY_DYNAMIC),
-                      ("rows_pull", moe.MOE_POLICY_ROWS),
-                      ("by_rank_pull", moe.MOE_POLICY_BY_RANK)):
+
+    def time_dispatch(pol, waves=0):
         def run(tr=None):
             moe.moe_dispatch_ex(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
                                 lay.row_src, regions.table,
                                 sregions.table if fp8 else None, regions.cap, lay.workspace,
-                                lay.status, policy=pol, trace=tr, scale_pitch=spitch)
+                                lay.status, policy=pol, trace=tr, scale_pitch=spitch,
+                                waves=waves)
         for _ in range(3):
             run()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -189,8 +188,28 @@ def ablation(a):
         us = e0.elapsed_time(e1) * 1e3 / a.steps
         rec = dict(dispatch_us=round(us, 2), GBps=round(b["dispatch"] / (us * 1e-6) / 1e9, 1))
         rec.update(trace_stats(trace, khz))
+        return rec
+
+    for name, pol in (("balanced_push", moe.MOE_POLICY_BALANCED),
+                      ("dynamic_push", moe.MOE_POLICY_DYNAMIC),
+                      ("rows_pull", moe.MOE_POLICY_ROWS),
+                      ("by_rank_pull", moe.MOE_POLICY_BY_RANK)):
+        rec = time_dispatch(pol)
         out["policies"][name] = rec
         print(f"[ablation] {name}: {rec}", file=sys.stderr, flush=True)
+    # wavefront-count sweep: 4 wavefronts per workgroup, so W wavefronts
+    # occupy up to W/4 compute units
+    out["wave_sweep"] = []
+    for waves in (R, 2 * R, 4 * R, 8 * R, 16 * R):
+        if moe.MOE_PLAN_PARTS % waves or waves % 4:
+            continue
+        rec = {"waves": waves}
+        for name, pol in (("balanced_push", moe.MOE_POLICY_BALANCED),
+                          ("by_rank_pull", moe.MOE_POLICY_BY_RANK)):
+            r = time_dispatch(pol, waves)
+            rec[name] = {k2: r[k2] for k2 in ("dispatch_us", "GBps", "completion_gap_pct")}
+        out["wave_sweep"].append(rec)
+        print(f"[ablation] sweep {rec}", file=sys.stderr, flush=True)
     # combine: static vs dynamic part assignment (expert outputs = the rows)
     w_d = torch.from_numpy(inp["topk_w"]).to(dev)
     if not fp8:
@@ -234,6 +253,8 @@ def main(argv=None):
                     help="instead of the step benchmark: dispatch under each work split")
     ap.add_argument("--ll", type=float, default=None, metavar="F",
                     help="fixed-capacity layout with windows of F x the mean expert load")
+    ap.add_argument("--cold-reps", type=int, default=20,
+                    help="repetitions of the cold-cache pass (0 skips it)")
     ap.add_argument("--graph", action="store_true",
                     help="capture each step in a graph (needs --ll: no host sync in a step)")
     a = ap.parse_args(argv)
@@ -405,6 +426,39 @@ def main(argv=None):
                      "traffic": traffic},
         "cpu_baseline": None,
     }
+    if graph is None and a.cold_reps > 0:
+        # Cold caches: before each operation write a 1 GiB buffer, which
+        # evicts the 256 MB MALL and the L2s, then time the operation alone.
+        fl = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        evc = [[torch.cuda.Event(enable_timing=True) for _ in range(6)]
+               for _ in range(a.cold_reps)]
+        for i, e in enumerate(evc):
+            for j, op in enumerate((lambda: lay.run(idx_d), dispatch, combine)):
+                fl.fill_((3 * i + j) & 0xFF)
+                e[2 * j].record(stream)
+                op()
+                e[2 * j + 1].record(stream)
+        torch.cuda.synchronize()
+        del fl
+
+        def pct(v):
+            return {"median": round(float(np.median(v)), 2),
+                    "p10": round(float(np.percentile(v, 10)), 2),
+                    "p90": round(float(np.percentile(v, 90)), 2)}
+        cl = np.array([e[0].elapsed_time(e[1]) for e in evc]) * 1e3
+        cd = np.array([e[2].elapsed_time(e[3]) for e in evc]) * 1e3
+        cc = np.array([e[4].elapsed_time(e[5]) for e in evc]) * 1e3
+        dcm = float(np.median(cd)) + float(np.median(cc))
+        out["cold"] = {"reps": a.cold_reps, "layout_us": pct(cl), "dispatch_us": pct(cd),
+                       "combine_us": pct(cc),
+                       "dispatch_plus_combine_GBps": round(dc_bytes / (dcm * 1e-6) / 1e9, 1)}
+        out["warm_median_us"] = {"layout": round(float(np.median(lay_ms)) * 1e3, 2),
+                                 "dispatch": round(float(np.median(dis_ms)) * 1e3, 2),
+                                 "combine": round(float(np.median(com_ms)) * 1e3, 2)}
+        if int(lay.status.item()) != 0:
+            print("[bench] status word set in the cold pass", file=sys.stderr)
+            return 1
+
     # Achievable-bandwidth reference on the same GPU: a plain device copy of
     # 1 GiB (read + write bytes / time), next to the 8 TB/s peak.
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)

@@ -215,6 +215,12 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
  *              the workspace (moe_layout zeroes it; the last wavefront resets
  *              it), so faster wavefronts take more parts.  Calls that share a
  *              workspace must not run concurrently under this policy.
+ * waves        wavefronts to launch: 0 launches as many as the device holds
+ *              at once (the product choice); otherwise a multiple of 4 that
+ *              divides MOE_PLAN_PARTS (and, under MOE_POLICY_BY_RANK, a
+ *              multiple of R), else MOE_EINVAL.  Fewer wavefronts occupy fewer
+ *              compute units: sweeping the count shows how each split's
+ *              balance depends on the number of cores sharing the work.
  * trace        NULL, or a device buffer of 2*trace_waves uint64: wavefront g
  *              (g < trace_waves) writes trace[2g] = its start time and
  *              trace[2g+1] = the time its last store completed, both from the
@@ -228,7 +234,7 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
                     const int32_t* rank_offset, const int32_t* row_src, const uint64_t* recv_x,
                     const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
                     const void* workspace, size_t workspace_bytes, uint32_t* status,
-                    int policy, uint64_t* trace, int trace_waves, void* stream);
+                    int policy, int waves, uint64_t* trace, int trace_waves, void* stream);
 
 /*
  * moe_combine -- gather each token's expert outputs back to token order and
@@ -253,14 +259,15 @@ int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H,
 
 /*
  * moe_combine_ex -- moe_combine with a work split (MOE_POLICY_BALANCED or
- * MOE_POLICY_DYNAMIC, as for moe_dispatch_ex; others are MOE_EINVAL) and the
- * optional per-wavefront trace of moe_dispatch_ex (same layout and clock).
+ * MOE_POLICY_DYNAMIC, as for moe_dispatch_ex; others are MOE_EINVAL), the
+ * wavefront count and the optional per-wavefront trace of moe_dispatch_ex
+ * (same rules, layout and clock).
  */
 int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
                    int E, int R, const int32_t* topk_idx, const int32_t* pos,
                    const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
                    const void* workspace, size_t workspace_bytes, uint32_t* status,
-                   int policy, uint64_t* trace, int trace_waves, void* stream);
+                   int policy, int waves, uint64_t* trace, int trace_waves, void* stream);
 
 /*
  * moe_expert_scale -- stand-in expert for tests and benchmarks, not part of

@@ -42,6 +42,14 @@ thread_local int g_last_hip_error = 0;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// An explicit wavefront count must split the plan into whole parts and
+// launch whole workgroups.
+bool waves_ok(int waves) {
+  if (waves == 0) return true;
+  return waves >= moe::kWavesPerBlock && waves <= MOE_PLAN_PARTS &&
+         waves % moe::kWavesPerBlock == 0 && MOE_PLAN_PARTS % waves == 0;
+}
+
 int shape_ok(int64_t T, int k, int E, int R) {
   if (T < 0 || k < 1 || k > MOE_MAX_K || E < 1 || E > MOE_MAX_EXPERTS || R < 1 || k > E ||
       E % R != 0)
@@ -132,7 +140,8 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
                     const int32_t* rank_offset, const int32_t* row_src, const uint64_t* recv_x,
                     const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
                     const void* workspace, size_t workspace_bytes, uint32_t* status,
-                    int policy, uint64_t* trace, int trace_waves, void* stream) {
+                    int policy, int waves, uint64_t* trace, int trace_waves,
+                    void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1 || (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3)) return MOE_EINVAL;
@@ -145,6 +154,8 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
     return MOE_EINVAL;
   const bool pull = policy == MOE_POLICY_ROWS || policy == MOE_POLICY_BY_RANK;
   if (pull && T > 0 && !row_src) return MOE_EINVAL;
+  if (!waves_ok(waves) || (waves && policy == MOE_POLICY_BY_RANK && waves % R != 0))
+    return MOE_EINVAL;
   if (trace && trace_waves < 0) return MOE_EINVAL;
   const int64_t row_bytes = fp8 ? (int64_t)H : 2 * (int64_t)H;
   if (row_bytes % 16 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
@@ -178,6 +189,7 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
                                           moe::layout_geom(T, E).ticket_offset);
   a.trace = trace;
   a.trace_waves = trace ? trace_waves : 0;
+  a.launch_waves = waves;
   return launched(moe::launch_dispatch(a, policy, as_stream(stream)));
 }
 
@@ -188,20 +200,22 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
                  uint32_t* status, void* stream) {
   return moe_dispatch_ex(x, x_scales, dtype, T, H, k, E, R, topk_idx, pos, rank_offset, nullptr,
                          recv_x, recv_scales, scale_pitch, recv_cap, workspace, workspace_bytes,
-                         status, MOE_POLICY_BALANCED, nullptr, 0, stream);
+                         status, MOE_POLICY_BALANCED, 0, nullptr, 0, stream);
 }
 
 int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
                    int E, int R, const int32_t* topk_idx, const int32_t* pos,
                    const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
                    const void* workspace, size_t workspace_bytes, uint32_t* status,
-                   int policy, uint64_t* trace, int trace_waves, void* stream) {
+                   int policy, int waves, uint64_t* trace, int trace_waves,
+                   void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1) return MOE_EINVAL;
   if (!expert_y || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
   if (T > 0 && (!topk_w || !topk_idx || !pos || !y)) return MOE_EINVAL;
   if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_DYNAMIC) return MOE_EINVAL;
+  if (!waves_ok(waves)) return MOE_EINVAL;
   if (trace && trace_waves < 0) return MOE_EINVAL;
   if ((2 * (int64_t)H) % 16 != 0 || !aligned(y, 16)) return MOE_EALIGN;
   if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
@@ -222,6 +236,7 @@ int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int
   a.status = status;
   a.trace = trace;
   a.trace_waves = trace ? trace_waves : 0;
+  a.launch_waves = waves;
   a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
                                           moe::layout_geom(T, E).ticket_offset) + 2;
   return launched(moe::launch_combine(a, policy, as_stream(stream)));
@@ -232,7 +247,7 @@ int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H,
                 const int32_t* recv_cap, uint16_t* y, const void* workspace,
                 size_t workspace_bytes, uint32_t* status, void* stream) {
   return moe_combine_ex(expert_y, topk_w, T, H, k, E, R, topk_idx, pos, rank_offset, recv_cap, y,
-                        workspace, workspace_bytes, status, MOE_POLICY_BALANCED, nullptr, 0,
+                        workspace, workspace_bytes, status, MOE_POLICY_BALANCED, 0, nullptr, 0,
                         stream);
 }
 

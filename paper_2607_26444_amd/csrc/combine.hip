@@ -192,7 +192,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
 template <int KW, bool DYN>
 hipError_t launch_kw(CombineArgs a, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&combine_kernel<KW, DYN>);
-  const int waves = resident_waves(fn, 0);
+  const int waves = a.launch_waves > 0 ? a.launch_waves : resident_waves(fn, 0);
   a.parts_per_wave = MOE_PLAN_PARTS / waves;
   hipLaunchKernelGGL((combine_kernel<KW, DYN>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
                      stream, a);

@@ -233,8 +233,8 @@ __global__ __launch_bounds__(kBlock) void dispatch_pull_kernel(DispatchArgs a) {
 template <int VPL, bool FULL, bool SCALES, int POLICY>
 hipError_t launch_pull(DispatchArgs a, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&dispatch_pull_kernel<VPL, FULL, SCALES, POLICY>);
-  int waves = resident_waves(fn, 0);
-  if (POLICY == MOE_POLICY_BY_RANK) {
+  int waves = a.launch_waves > 0 ? a.launch_waves : resident_waves(fn, 0);
+  if (POLICY == MOE_POLICY_BY_RANK && a.launch_waves == 0) {
     // whole groups per rank, and whole workgroups
     waves = waves / a.R * a.R;
     while (waves > a.R && waves % kWavesPerBlock != 0) waves -= a.R;
@@ -267,7 +267,7 @@ hipError_t launch_push(DispatchArgs a, hipStream_t stream) {
   const void* fn =
       full ? reinterpret_cast<const void*>(&dispatch_kernel<VPL, true, SCALES, DYN>)
            : reinterpret_cast<const void*>(&dispatch_kernel<VPL, false, SCALES, DYN>);
-  const int waves = resident_waves(fn, 0);
+  const int waves = a.launch_waves > 0 ? a.launch_waves : resident_waves(fn, 0);
   a.parts_per_wave = MOE_PLAN_PARTS / waves;
   const dim3 grid(waves / kWavesPerBlock), block(kBlock);
   if (full)

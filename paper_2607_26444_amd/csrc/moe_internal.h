@@ -68,6 +68,7 @@ struct DispatchArgs {
   const int32_t* recv_cap;
   const int32_t* bound;        // plan: bound[MOE_PLAN_PARTS + 1]
   int32_t parts_per_wave;      // MOE_PLAN_PARTS / launched wavefronts
+  int32_t launch_waves;        // wavefronts to launch; 0 = as many as are resident
   uint32_t* status;
   const int32_t* row_src;      // pull policies only
   int32_t R;
@@ -91,6 +92,7 @@ struct CombineArgs {
   uint16_t* y;
   const int32_t* bound;
   int32_t parts_per_wave;
+  int32_t launch_waves;
   uint32_t* status;
   uint64_t* trace;
   int32_t trace_waves;

@@ -83,9 +83,9 @@ def lib() -> ctypes.CDLL:
                                    P, P, SZ, P, P]
         L.moe_combine.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P, P]
         L.moe_dispatch_ex.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, P,
-                                      I32, P, P, SZ, P, I32, P, I32, P]
+                                      I32, P, P, SZ, P, I32, I32, P, I32, P]
         L.moe_combine_ex.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P,
-                                     I32, P, I32, P]
+                                     I32, I32, P, I32, P]
         L.moe_expert_scale.argtypes = [P, P, I32, I32, I32, I32, I32, I32, P, P, P, P, I64, P]
         for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
                   "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale"):
@@ -159,24 +159,25 @@ def moe_dispatch(x, x_scales, dtype, H, E, R, topk_idx, pos, rank_offset, recv_x
 
 def moe_dispatch_ex(x, x_scales, dtype, H, E, R, topk_idx, pos, rank_offset, row_src,
                     recv_x, recv_scales, recv_cap, workspace, status, policy=MOE_POLICY_BALANCED,
-                    trace=None, stream=None, scale_pitch=0):
+                    trace=None, stream=None, scale_pitch=0, waves=0):
     T, k = topk_idx.shape
     _check("moe_dispatch_ex", lib().moe_dispatch_ex(
         _ptr(x), _ptr(x_scales), dtype, T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
         _ptr(rank_offset), _ptr(row_src), _ptr(recv_x), _ptr(recv_scales), scale_pitch,
         _ptr(recv_cap), _ptr(workspace), workspace.numel() * workspace.element_size(),
-        _ptr(status), policy, _ptr(trace), 0 if trace is None else trace.numel() // 2,
+        _ptr(status), policy, waves, _ptr(trace), 0 if trace is None else trace.numel() // 2,
         _stream(stream)))
 
 
 def moe_combine_ex(expert_y, topk_w, H, E, R, topk_idx, pos, rank_offset, recv_cap, y,
-                   workspace, status, policy=MOE_POLICY_BALANCED, trace=None, stream=None):
+                   workspace, status, policy=MOE_POLICY_BALANCED, trace=None, stream=None,
+                   waves=0):
     T, k = topk_idx.shape
     _check("moe_combine_ex", lib().moe_combine_ex(
         _ptr(expert_y), _ptr(topk_w), T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
         _ptr(rank_offset), _ptr(recv_cap), _ptr(y), _ptr(workspace),
-        workspace.numel() * workspace.element_size(), _ptr(status), policy, _ptr(trace),
-        0 if trace is None else trace.numel() // 2, _stream(stream)))
+        workspace.numel() * workspace.element_size(), _ptr(status), policy, waves,
+        _ptr(trace), 0 if trace is None else trace.numel() // 2, _stream(stream)))
 
 
 def moe_combine(expert_y, topk_w, H, E, R, topk_idx, pos, rank_offset, recv_cap, y,

@@ -41,7 +41,7 @@ class GpuRun:
 
     def __init__(self, cfg, inp, topk_idx=None, topk_w=None, spare_rows=0,
                  cap_delta=None, identity=None, combine_on_dispatch=False, scale_pitch=None,
-                 policy=0, trace=False, combine_policy=0, repeat=1, capacity=None):
+                 policy=0, trace=False, combine_policy=0, repeat=1, capacity=None, waves=0):
         self.cfg = cfg
         T, H, E, R = cfg["T"], cfg["H"], cfg["E"], cfg["R"]
         idx = inp["topk_idx"] if topk_idx is None else topk_idx
@@ -87,7 +87,7 @@ class GpuRun:
                                 lay.row_src, self.regions.table,
                                 self.sregions.table if fp8 else None, cap_d, lay.workspace,
                                 lay.status, policy=policy, trace=self.dtrace,
-                                scale_pitch=self.scale_pitch)
+                                scale_pitch=self.scale_pitch, waves=waves)
 
         y = torch.empty((max(1, T), H), dtype=torch.int16, device="cuda")
         y.fill_(0x5A5A)
@@ -107,7 +107,7 @@ class GpuRun:
         for _ in range(repeat):
             moe.moe_combine_ex(ey_table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, cap_d,
                                y, lay.workspace, lay.status, policy=combine_policy,
-                               trace=self.ctrace)
+                               trace=self.ctrace, waves=waves)
         torch.cuda.synchronize()
 
         nrows = T * k if capacity is None else E * capacity

@@ -87,7 +87,7 @@ def _dispatch_args(**kw):
     n = moe.moe_layout_workspace_bytes(64, 8, 256, 64)
     a = dict(x=FAKE, xs=None, dtype=0, T=64, H=7168, k=8, E=256, R=64, idx=FAKE, pos=FAKE,
              ro=FAKE, rs=FAKE, rx=FAKE, rsc=None, pitch=0, cap=FAKE, ws=WS, wsb=n,
-             st=FAKE, policy=0, trace=None, tw=0, stream=None)
+             st=FAKE, policy=0, waves=0, trace=None, tw=0, stream=None)
     a.update(kw)
     return list(a.values())
 
@@ -109,13 +109,16 @@ def test_dispatch_argument_errors():
     assert L.moe_dispatch_ex(*_dispatch_args(wsb=16)) == moe.MOE_EWORKSPACE
     assert L.moe_dispatch_ex(*_dispatch_args(rx=None)) == moe.MOE_EINVAL
     assert L.moe_dispatch_ex(*_dispatch_args(trace=FAKE, tw=-1)) == moe.MOE_EINVAL
+    for w in (-4, 2, 6, 20, 12292, 24576):             # not a divisor of the plan / of 4
+        assert L.moe_dispatch_ex(*_dispatch_args(waves=w)) == moe.MOE_EINVAL
+    assert L.moe_dispatch_ex(*_dispatch_args(policy=2, rs=FAKE, waves=96)) == moe.MOE_EINVAL
 
 
 def test_combine_argument_errors():
     L = moe.lib()
     n = moe.moe_layout_workspace_bytes(64, 8, 256, 64)
-    ok = [FAKE, FAKE, 64, 7168, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, WS, n, FAKE, 0, None,
-          0, None]
+    ok = [FAKE, FAKE, 64, 7168, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, WS, n, FAKE, 0, 0,
+          None, 0, None]
     bad = list(ok); bad[11] = MIS                      # y misaligned
     assert L.moe_combine_ex(*bad) == moe.MOE_EALIGN
     bad = list(ok); bad[0] = None                      # null expert table
@@ -125,6 +128,8 @@ def test_combine_argument_errors():
     bad = list(ok); bad[4] = 300                       # k > MOE_MAX_K
     assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
     bad = list(ok); bad[15] = moe.MOE_POLICY_ROWS      # pull splits are dispatch-only
+    assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
+    bad = list(ok); bad[16] = 100                      # does not divide the plan
     assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
 
 

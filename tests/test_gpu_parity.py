@@ -30,7 +30,7 @@ def _h():
 
 def _full_parity(cfg, inp=None, idx=None, w=None, spare_rows=2, cap_delta=None,
                  identity=None, scale_pitch=None, policy=0, trace=False, combine_policy=0,
-                 repeat=1, capacity=None):
+                 repeat=1, capacity=None, waves=0):
     h = _h()
     inp = wl.make_inputs(cfg) if inp is None else inp
     h.log(f"[parity] {cfg['name']} T={cfg['T']} H={cfg['H']} E={cfg['E']} R={cfg['R']} "
@@ -38,7 +38,7 @@ def _full_parity(cfg, inp=None, idx=None, w=None, spare_rows=2, cap_delta=None,
     run = h.GpuRun(cfg, inp, topk_idx=idx, topk_w=w, spare_rows=spare_rows,
                    cap_delta=cap_delta, identity=identity, scale_pitch=scale_pitch,
                    policy=policy, trace=trace, combine_policy=combine_policy, repeat=repeat,
-                   capacity=capacity)
+                   capacity=capacity, waves=waves)
     ref = h.oracle_chain(cfg, inp, topk_idx=idx, topk_w=w, caps=run.caps,
                          identity=identity, scale_pitch=run.scale_pitch, capacity=capacity)
     # layout: bit-exact
@@ -163,6 +163,16 @@ def test_dynamic_policy_matches_oracle(T, H, E, R, k, payload, mask):
     inp = wl.make_inputs(cfg)
     idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
     _full_parity(cfg, inp, idx=idx, policy=3, combine_policy=3, repeat=3)
+
+
+@pytest.mark.parametrize("policy,cpolicy", [(0, 0), (1, 0), (2, 0), (3, 3)])
+@pytest.mark.parametrize("waves", [64, 256, 3072])
+def test_explicit_wave_counts_match_oracle(policy, cpolicy, waves):
+    """Every work split gives the oracle's bytes and y at a chosen wavefront
+    count, below and above what the device holds at once."""
+    T, H, E, R, k = 2500, 1536, 64, 16, 6
+    cfg = wl.custom(T, H, E, R, k, zipf_s=1.2, seed=waves + policy)
+    _full_parity(cfg, policy=policy, combine_policy=cpolicy, waves=waves, repeat=2)
 
 
 @pytest.mark.parametrize("T,H,E,R,k,payload,C,zipf", [
