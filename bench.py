@@ -47,10 +47,12 @@ def algorithmic_bytes(cfg) -> dict:
     return dict(dispatch=dispatch, combine=combine, row=row, n=n)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kernel: str) -> str:
+    """Hash of the device code of one kernel: its source file and the shared
+    device header."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_26444_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in (f"{kernel}.hip", "moe_internal.h"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -67,7 +69,7 @@ def read_traffic(workload: str, kernel: str):
         if ":" in line and not line.startswith("#"):
             a, b = line.split(":", 1)
             kv[a.strip()] = b.strip()
-    if kv.get("source_hash") != kernel_source_hash():
+    if kv.get("source_hash") != kernel_source_hash(kernel):
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
