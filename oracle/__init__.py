@@ -52,8 +52,14 @@ def lib():
                                           P_, P_]
         L.oracle_combine.argtypes = [P_, P_, I64, I32, I32, I32, I32, P_, P_, P_,
                                      P_, P_, P_]
+        L.oracle_layout_dedup.argtypes = [P_, I64, I32, I32, I32, P_, P_, P_, P_, P_]
+        L.oracle_expand.argtypes = [P_, P_, I64, I64, I64, I64, I32, I32, I32, P_, P_, P_,
+                                    P_, P_, P_, P_, P_, P_, P_]
+        L.oracle_combine_local.argtypes = [P_, P_, I64, I32, I32, I32, I32, P_, P_, P_, P_,
+                                           P_, P_, P_, P_, P_]
         for f in ("oracle_layout", "oracle_layout_fixed", "oracle_plan", "oracle_dispatch",
-                  "oracle_expert_scale", "oracle_combine"):
+                  "oracle_expert_scale", "oracle_combine", "oracle_layout_dedup",
+                  "oracle_expand", "oracle_combine_local"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -205,3 +211,87 @@ def combine(expert_y, topk_w, topk_idx, pos, rank_offset, recv_cap, E: int,
                               _p(pos), _p(ro), _p(cap), _p(y), _p(st))
     _check(rc, "oracle_combine")
     return y, int(st[0])
+
+
+
+# ---------------------------------------------------------------- per-peer deduplication
+def layout_dedup(topk_idx: np.ndarray, E: int, R: int) -> dict:
+    """One row per (token, peer) pair: tok_count, tok_offset, tok_pos, tok_src."""
+    idx = np.ascontiguousarray(topk_idx, dtype=np.int32)
+    T, k = idx.shape
+    out = dict(tok_count=np.zeros(R, np.int32), tok_offset=np.zeros(R + 1, np.int32),
+               tok_pos=np.zeros(T * k, np.int32), tok_src=np.zeros(T * k, np.int32))
+    st = np.zeros(1, np.uint32)
+    rc = lib().oracle_layout_dedup(_p(idx), T, k, E, R, _p(out["tok_count"]),
+                                   _p(out["tok_offset"]), _p(out["tok_pos"]),
+                                   _p(out["tok_src"]), _p(st))
+    _check(rc, "oracle_layout_dedup")
+    out["status"] = int(st[0])
+    return out
+
+
+def dispatch_dedup(x_rows, x_scale_rows, topk_idx, tok_pos, tok_offset, E: int, R: int,
+                   dedup_cap, sentinel: int = 0xA5, scale_pitch: int = 0):
+    """Send each (token, peer) pair once: the per-slot copy of dispatch()
+    applied to the pair rows (tok_pos is -1 on all but a pair's first slot)."""
+    return dispatch(x_rows, x_scale_rows, topk_idx, tok_pos, tok_offset, E, R, dedup_cap,
+                    sentinel=sentinel, scale_pitch=scale_pitch)
+
+
+def expand(dedup_regions, dedup_scale_regions, scale_row_bytes: int, topk_idx, pos,
+           rank_offset, tok_pos, tok_offset, dedup_cap, E: int, R: int, recv_cap,
+           sentinel: int = 0xA5):
+    """Receiver-side permutation of pair rows into expert order.  Regions
+    are uint8 [rows, row_bytes]; scale regions uint8 [rows, pitch], the pitch
+    being their width.  Returns (regions, scale_regions or None, status)."""
+    idx = np.ascontiguousarray(topk_idx, dtype=np.int32)
+    T, k = idx.shape
+    dregs = [np.ascontiguousarray(a, dtype=np.uint8) for a in dedup_regions]
+    rb = dregs[0].shape[1]
+    cap = np.ascontiguousarray(recv_cap, dtype=np.int32)
+    dcap = np.ascontiguousarray(dedup_cap, dtype=np.int32)
+    regs = [np.full((int(c), rb), sentinel, np.uint8) for c in cap]
+    dsregs, sregs, pitch = None, None, 0
+    if dedup_scale_regions is not None:
+        dsregs = [np.ascontiguousarray(a, dtype=np.uint8) for a in dedup_scale_regions]
+        pitch = dsregs[0].shape[1]
+        sregs = [np.full((int(c), pitch), sentinel, np.uint8) for c in cap]
+    pos, ro, tp, to = (np.ascontiguousarray(a, dtype=np.int32)
+                       for a in (pos, rank_offset, tok_pos, tok_offset))
+    st = np.zeros(1, np.uint32)
+    rc = lib().oracle_expand(_ptr_table(dregs),
+                             _ptr_table(dsregs) if dsregs is not None else None,
+                             rb, scale_row_bytes, pitch, T, k, E, R, _p(idx), _p(pos), _p(ro),
+                             _p(tp), _p(to), _p(dcap), _ptr_table(regs),
+                             _ptr_table(sregs) if sregs is not None else None, _p(cap),
+                             _p(st))
+    _check(rc, "oracle_expand")
+    return regs, sregs, int(st[0])
+
+
+def combine_local(expert_y, topk_w, topk_idx, pos, rank_offset, recv_cap, tok_pos,
+                  tok_offset, part_cap, E: int, R: int, H: int, sentinel: int = 0xA5A5):
+    """Per-(token, peer) partial sums: regions uint16 [part_cap[r], H]
+    (rows no pair writes keep `sentinel`).  Returns (partials, status)."""
+    idx = np.ascontiguousarray(topk_idx, dtype=np.int32)
+    T, k = idx.shape
+    w = np.ascontiguousarray(topk_w, dtype=np.float32)
+    pos, ro, cap, tp, to, pc = (np.ascontiguousarray(a, dtype=np.int32)
+                                for a in (pos, rank_offset, recv_cap, tok_pos, tok_offset,
+                                          part_cap))
+    ys = [np.ascontiguousarray(a, dtype=np.uint16) for a in expert_y]
+    parts = [np.full((int(c), H), sentinel, np.uint16) for c in pc]
+    st = np.zeros(1, np.uint32)
+    rc = lib().oracle_combine_local(_ptr_table(ys), _p(w), T, H, k, E, R, _p(idx), _p(pos),
+                                    _p(ro), _p(cap), _p(tp), _p(to), _p(pc),
+                                    _ptr_table(parts), _p(st))
+    _check(rc, "oracle_combine_local")
+    return parts, int(st[0])
+
+
+def combine_dedup(partials, topk_idx, tok_pos, tok_offset, part_cap, E: int, R: int, H: int):
+    """Source side of the deduplicated combine: the sum of a token's peer
+    partials, i.e. combine() with unit weights over the pair rows."""
+    T, k = np.asarray(topk_idx).shape
+    return combine(partials, np.ones((T, k), np.float32), topk_idx, tok_pos, tok_offset,
+                   part_cap, E, R, H)

@@ -343,4 +343,161 @@ int oracle_combine(uint16_t* const* expert_y, const float* topk_w, int64_t T,
   return 0;
 }
 
+// ---------------------------------------------------------------------------
+// Per-peer deduplicated placement (the peer windows of Appendix D, with each
+// token sent once to every peer that hosts at least one of its experts --
+// the reading taken for traffic that Section 6.2 calls uneven per peer).
+// A token's routed slots (the same unused-slot rules as oracle_layout) are
+// grouped by peer r = e / (E/R); the first slot of each group carries the
+// group's row in peer window r, later slots of the group carry -1.  Rows of
+// one peer window are in token order.
+//
+// Outputs: tok_count[R] (tokens sent to peer r), tok_offset[R+1] (exclusive
+// prefix sums), tok_pos[T*k] (global row of the slot's (token, peer) pair on
+// the group's first slot, -1 elsewhere), tok_src[T*k] (slot t*k+j of the
+// first slot of each row, -1 past the last row).  status |= bits 1, 2.
+// ---------------------------------------------------------------------------
+int oracle_layout_dedup(const int32_t* topk_idx, int64_t T, int32_t k, int32_t E, int32_t R,
+                        int32_t* tok_count, int32_t* tok_offset, int32_t* tok_pos,
+                        int32_t* tok_src, uint32_t* status) {
+  if (T < 0 || k < 1 || E < 1 || R < 1 || E % R != 0) return -1;
+  const int32_t L = E / R;
+  const int64_t S = T * k;
+  uint32_t st = 0;
+  // first[s]: slot s is routed and no earlier routed slot of its token has
+  // an expert on the same peer
+  std::vector<char> first((size_t)S, 0);
+  for (int64_t t = 0; t < T; ++t) {
+    std::vector<char> used((size_t)k, 0);
+    for (int32_t j = 0; j < k; ++j) {
+      const int32_t e = topk_idx[t * k + j];
+      if (e == -1) continue;
+      if (e < -1 || e >= E) { st |= kBadIndex; continue; }
+      bool repeat = false;
+      for (int32_t jj = 0; jj < j; ++jj)
+        if (topk_idx[t * k + jj] == e) repeat = true;
+      if (repeat) { st |= kDupIndex; continue; }
+      used[(size_t)j] = 1;
+      bool seen = false;
+      for (int32_t jj = 0; jj < j; ++jj)
+        if (used[(size_t)jj] && topk_idx[t * k + jj] / L == e / L) seen = true;
+      first[(size_t)(t * k + j)] = seen ? 0 : 1;
+    }
+  }
+  for (int32_t r = 0; r < R; ++r) tok_count[r] = 0;
+  for (int64_t s = 0; s < S; ++s)
+    if (first[(size_t)s]) tok_count[topk_idx[s] / L] += 1;
+  tok_offset[0] = 0;
+  for (int32_t r = 0; r < R; ++r) tok_offset[r + 1] = tok_offset[r] + tok_count[r];
+  std::vector<int32_t> next(tok_offset, tok_offset + R);
+  for (int64_t s = 0; s < S; ++s) tok_src[s] = -1;
+  for (int64_t s = 0; s < S; ++s) {     // s = t*k + j ascending: token order
+    if (!first[(size_t)s]) { tok_pos[s] = -1; continue; }
+    const int32_t p = next[topk_idx[s] / L]++;
+    tok_pos[s] = p;
+    tok_src[p] = (int32_t)s;
+  }
+  *status |= st;
+  return 0;
+}
+
+// Row of the (token, peer) pair of slot s = t*k + j in the deduplicated
+// placement: tok_pos of the first slot of token t whose expert is on the same
+// peer and that carries a row; -1 if there is none.
+static int32_t pair_row(const int32_t* topk_idx, const int32_t* tok_pos, int64_t t, int32_t j,
+                        int32_t k, int32_t L) {
+  const int32_t r = topk_idx[t * k + j] / L;
+  for (int32_t jj = 0; jj <= j; ++jj) {
+    const int64_t s = t * k + jj;
+    if (tok_pos[s] >= 0 && topk_idx[s] / L == r) return tok_pos[s];
+  }
+  return -1;
+}
+
+// ---------------------------------------------------------------------------
+// Receiver-side expert permutation after a deduplicated dispatch: every
+// routed slot (t, j) with expert e on peer r gets the row of its (token,
+// peer) pair, copied from the deduplicated region r (row pair_row -
+// tok_offset[r]) to the expert-ordered region r at row pos[t,j] -
+// rank_offset[r] -- the same place a per-slot dispatch writes, so the result
+// is that of oracle_dispatch.  fp8 scale rows are copied the same way, their
+// pitch padding set to zero.  A source row at or past dedup_cap[r] or a
+// destination row at or past recv_cap[r] is skipped and sets status bit 4.
+// ---------------------------------------------------------------------------
+int oracle_expand(uint8_t* const* dedup_x, uint8_t* const* dedup_s, int64_t row_bytes,
+                  int64_t scale_row_bytes, int64_t scale_pitch, int64_t T, int32_t k, int32_t E,
+                  int32_t R, const int32_t* topk_idx, const int32_t* pos,
+                  const int32_t* rank_offset, const int32_t* tok_pos, const int32_t* tok_offset,
+                  const int32_t* dedup_cap, uint8_t* const* recv_x, uint8_t* const* recv_s,
+                  const int32_t* recv_cap, uint32_t* status) {
+  if (T < 0 || k < 1 || E < 1 || R < 1 || E % R != 0) return -1;
+  const int32_t L = E / R;
+  uint32_t st = 0;
+  for (int64_t t = 0; t < T; ++t) {
+    for (int32_t j = 0; j < k; ++j) {
+      const int32_t p = pos[t * k + j];
+      if (p < 0) continue;
+      const int32_t r = topk_idx[t * k + j] / L;
+      const int32_t q = pair_row(topk_idx, tok_pos, t, j, k, L);
+      if (q < 0) continue;
+      const int64_t src = (int64_t)q - tok_offset[r], dst = (int64_t)p - rank_offset[r];
+      if (src >= dedup_cap[r] || dst >= recv_cap[r]) { st |= kCapacity; continue; }
+      std::memcpy(recv_x[r] + dst * row_bytes, dedup_x[r] + src * row_bytes, (size_t)row_bytes);
+      if (dedup_s) {
+        uint8_t* srow = recv_s[r] + dst * scale_pitch;
+        std::memcpy(srow, dedup_s[r] + src * scale_pitch, (size_t)scale_row_bytes);
+        std::memset(srow + scale_row_bytes, 0, (size_t)(scale_pitch - scale_row_bytes));
+      }
+    }
+  }
+  *status |= st;
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Receiver-side partial combine after a deduplicated dispatch: for every
+// (token, peer) pair, the top-k-weighted sum of the token's expert outputs on
+// that peer, j ascending, in double, rounded once to bf16 and written to row
+// pair_row - tok_offset[r] of the peer's partial region (the row that goes
+// back to the token's source).  Expert-output rows are addressed as in
+// oracle_combine.  The source then adds the partials of a token's peers
+// (oracle_combine with unit weights over the pair rows).  Skipped rows set
+// status bit 4: expert rows at or past recv_cap[r] (not summed) and pair
+// rows at or past part_cap[r] (not written).
+// ---------------------------------------------------------------------------
+int oracle_combine_local(uint16_t* const* expert_y, const float* topk_w, int64_t T, int32_t H,
+                         int32_t k, int32_t E, int32_t R, const int32_t* topk_idx,
+                         const int32_t* pos, const int32_t* rank_offset,
+                         const int32_t* recv_cap, const int32_t* tok_pos,
+                         const int32_t* tok_offset, const int32_t* part_cap,
+                         uint16_t* const* partial, uint32_t* status) {
+  if (T < 0 || H < 1 || k < 1 || E < 1 || R < 1 || E % R != 0) return -1;
+  const int32_t L = E / R;
+  uint32_t st = 0;
+  std::vector<double> acc((size_t)H);
+  for (int64_t t = 0; t < T; ++t) {
+    for (int32_t j0 = 0; j0 < k; ++j0) {
+      const int32_t q = tok_pos[t * k + j0];
+      if (q < 0) continue;                 // not the first slot of a pair
+      const int32_t r = topk_idx[t * k + j0] / L;
+      for (int32_t h = 0; h < H; ++h) acc[(size_t)h] = 0.0;
+      for (int32_t j = j0; j < k; ++j) {
+        const int32_t p = pos[t * k + j];
+        if (p < 0 || topk_idx[t * k + j] / L != r) continue;
+        const int64_t local = (int64_t)p - rank_offset[r];
+        if (local >= recv_cap[r]) { st |= kCapacity; continue; }
+        const uint16_t* row = expert_y[r] + local * H;
+        const double w = (double)topk_w[t * k + j];
+        for (int32_t h = 0; h < H; ++h) acc[(size_t)h] += w * oracle_bf16_to_double(row[h]);
+      }
+      const int64_t dst = (int64_t)q - tok_offset[r];
+      if (dst >= part_cap[r]) { st |= kCapacity; continue; }
+      uint16_t* o = partial[r] + dst * H;
+      for (int32_t h = 0; h < H; ++h) o[h] = oracle_bf16_from_double(acc[(size_t)h]);
+    }
+  }
+  *status |= st;
+  return 0;
+}
+
 }  // extern "C"

@@ -608,4 +608,268 @@ def pin_expert_scale_matches_torch():
                 assert np.array_equal(ey[r][i], want.astype(np.uint16)), (payload, r, i)
 
 
+
+# ------------------------------------------------------ per-peer deduplication
+def layout_dedup_bruteforce(idx: np.ndarray, E: int, R: int) -> dict:
+    """Deduplicated placement from its definition: the routed (token, peer)
+    pairs, each pair's row = number of pairs with a smaller (peer, token)
+    key, carried by the pair's first routed slot.  Quadratic; small inputs."""
+    T, k = idx.shape
+    L = E // R
+    st = 0
+    first_slot = {}                       # (r, t) -> first routed slot j
+    for t in range(T):
+        seen = set()
+        for j in range(k):
+            e = int(idx[t, j])
+            if e == -1:
+                continue
+            if e < -1 or e >= E:
+                st |= 1
+                continue
+            if e in seen:
+                st |= 2
+                continue
+            seen.add(e)
+            first_slot.setdefault((e // L, t), j)
+    keys = list(first_slot)
+    tok_pos = -np.ones(T * k, np.int64)
+    tok_src = -np.ones(T * k, np.int64)
+    for (r, t), j in first_slot.items():
+        row = sum(1 for key in keys if key < (r, t))
+        tok_pos[t * k + j] = row
+        tok_src[row] = t * k + j
+    cnt = np.array([sum(1 for key in keys if key[0] == r) for r in range(R)])
+    off = np.concatenate([[0], np.cumsum(cnt)])
+    return dict(tok_count=cnt, tok_offset=off, tok_pos=tok_pos, tok_src=tok_src, status=st)
+
+
+def _assert_dedup_equal(got, want, ctx):
+    for key in ("tok_count", "tok_offset", "tok_pos", "tok_src", "status"):
+        assert np.array_equal(np.asarray(got[key], np.int64),
+                              np.asarray(want[key], np.int64)), (key, ctx)
+
+
+def pin_layout_dedup_exhaustive_tiny():
+    """Every routing of 2 tokens x 2 slots over 4 experts on 2 peers, with
+    unused (-1), out-of-range (-3, -2, 4) and repeated indices."""
+    vals = [-3, -2, -1, 0, 1, 2, 3, 4]
+    for combo in itertools.product(vals, repeat=4):
+        idx = np.array(combo, np.int32).reshape(2, 2)
+        got = oracle.layout_dedup(idx, 4, 2)
+        _assert_dedup_equal(got, layout_dedup_bruteforce(idx, 4, 2), combo)
+
+
+def pin_layout_dedup_random_bruteforce():
+    """Random routings with masks, repeats and bad indices, several E/R."""
+    rng = np.random.default_rng(31)
+    for (T, k, E, R) in ((17, 3, 12, 3), (9, 5, 16, 4), (25, 4, 8, 8), (11, 6, 24, 2),
+                         (13, 2, 6, 1)):
+        idx = rng.integers(-3, E + 1, size=(T, k)).astype(np.int32)
+        got = oracle.layout_dedup(idx, E, R)
+        _assert_dedup_equal(got, layout_dedup_bruteforce(idx, E, R), (T, k, E, R))
+
+
+def pin_layout_dedup_invariants_and_special_cases():
+    """Peer counts are the numbers of distinct tokens per peer (numpy sets);
+    with one expert per peer the deduplicated placement is the per-expert one;
+    with k = 1 every slot is its own pair and the counts are the peer loads."""
+    for cfg in (wl.custom(500, 64, 32, 8, 6, zipf_s=1.2, seed=41),
+                wl.custom(300, 64, 16, 16, 4, seed=42),
+                wl.custom(200, 64, 24, 6, 1, seed=43)):
+        inp = wl.make_inputs(cfg)
+        idx = wl.mask_slots(inp["topk_idx"], 0.1, seed=44)
+        E, R, (T, k) = cfg["E"], cfg["R"], idx.shape
+        L = E // R
+        d = oracle.layout_dedup(idx, E, R)
+        lay = oracle.layout(idx, E, R)
+        for r in range(R):
+            toks = np.unique(np.nonzero(((idx // L) == r) & (idx >= 0))[0])
+            assert d["tok_count"][r] == len(toks)
+            rows = d["tok_pos"][(d["tok_pos"] >= d["tok_offset"][r]) &
+                                (d["tok_pos"] < d["tok_offset"][r + 1])]
+            assert np.array_equal(np.sort(d["tok_src"][rows] // k), toks)
+            # token order inside the peer window
+            assert np.all(np.diff(d["tok_src"][d["tok_offset"][r]:d["tok_offset"][r + 1]]) > 0)
+        assert np.all(d["tok_count"] <= lay["rank_count"])
+        n = int(d["tok_offset"][-1])
+        assert np.array_equal(np.sort(d["tok_pos"][d["tok_pos"] >= 0]), np.arange(n))
+        if L == 1 or k == 1:
+            assert np.array_equal(d["tok_count"], lay["rank_count"])
+        if L == 1:
+            assert np.array_equal(d["tok_pos"], lay["pos"])
+
+
+def _dedup_chain(cfg, idx, w, identity, scale_pitch=0, dcap_delta=None):
+    inp = wl.make_inputs(cfg)
+    E, R, H = cfg["E"], cfg["R"], cfg["H"]
+    fp8 = cfg["payload"] == wl.FP8_E4M3
+    xs = _rows_u8(inp["x_scales"]) if fp8 else None
+    lay = oracle.layout(idx, E, R)
+    d = oracle.layout_dedup(idx, E, R)
+    dcap = d["tok_count"].copy()
+    if dcap_delta is not None:
+        dcap = np.maximum(0, dcap + np.asarray(dcap_delta))
+    dregs, dsregs, st_d = oracle.dispatch_dedup(_rows_u8(inp["x"]), xs, idx, d["tok_pos"],
+                                                d["tok_offset"], E, R, dcap,
+                                                scale_pitch=scale_pitch)
+    cap = lay["rank_count"]
+    srb = xs.shape[1] if fp8 else 0
+    regs, sregs, st_e = oracle.expand(dregs, dsregs, srb, idx, lay["pos"], lay["rank_offset"],
+                                      d["tok_pos"], d["tok_offset"], dcap, E, R, cap)
+    out = dict(inp=inp, lay=lay, d=d, dcap=dcap, dregs=dregs, dsregs=dsregs, regs=regs,
+               sregs=sregs, st_d=st_d, st_e=st_e)
+    ey = oracle.expert_scale(regs, sregs, fp8, H, E, R, identity, lay["expert_offset"],
+                             lay["rank_offset"], cap)
+    parts, st_l = oracle.combine_local(ey, w, idx, lay["pos"], lay["rank_offset"], cap,
+                                       d["tok_pos"], d["tok_offset"], d["tok_count"],
+                                       E, R, H)
+    y, st_y = oracle.combine_dedup(parts, idx, d["tok_pos"], d["tok_offset"],
+                                   d["tok_count"], E, R, H)
+    out.update(ey=ey, parts=parts, y=y, st_l=st_l, st_y=st_y)
+    return out
+
+
+def pin_dispatch_dedup_rows_and_expand_equals_dispatch():
+    """Pair rows hold their token's row; expanding them into expert order
+    gives byte for byte the per-slot dispatch (bf16, fp8 with packed and
+    pitched scale rows, masked slots)."""
+    for cfg, pitch in ((wl.custom(300, 72, 32, 8, 6, zipf_s=1.2, seed=51), 0),
+                       (wl.custom(150, 256, 24, 6, 4, payload=wl.FP8_E4M3, seed=52), 0),
+                       (wl.custom(150, 256, 24, 6, 4, payload=wl.FP8_E4M3, seed=53), 64)):
+        inp0 = wl.make_inputs(cfg)
+        idx = wl.mask_slots(inp0["topk_idx"], 0.15, seed=54)
+        c = _dedup_chain(cfg, idx, inp0["topk_w"], True, scale_pitch=pitch)
+        E, R = cfg["E"], cfg["R"]
+        assert c["st_d"] == 0 and c["st_e"] == 0
+        k = idx.shape[1]
+        xr = _rows_u8(c["inp"]["x"])
+        for r in range(R):
+            a, b = c["d"]["tok_offset"][r], c["d"]["tok_offset"][r + 1]
+            assert np.array_equal(c["dregs"][r], xr[c["d"]["tok_src"][a:b] // k])
+        fp8 = cfg["payload"] == wl.FP8_E4M3
+        xs = _rows_u8(c["inp"]["x_scales"]) if fp8 else None
+        regs, sregs, st = oracle.dispatch(xr, xs, idx, c["lay"]["pos"], c["lay"]["rank_offset"],
+                                          E, R, c["lay"]["rank_count"], scale_pitch=pitch)
+        for r in range(R):
+            assert np.array_equal(c["regs"][r], regs[r]), r
+            if fp8:
+                assert np.array_equal(c["sregs"][r], sregs[r]), r
+
+
+def _pair_routing(T, k, E, R, seed):
+    """Each token picks k/2 peers and both of two distinct experts on each."""
+    rng = np.random.default_rng(seed)
+    L = E // R
+    idx = np.zeros((T, k), np.int32)
+    for t in range(T):
+        peers = rng.choice(R, size=k // 2, replace=False)
+        col = []
+        for r in peers:
+            col.extend(r * L + rng.choice(L, size=2, replace=False))
+        idx[t] = rng.permutation(np.array(col, np.int32))
+    return idx
+
+
+def pin_dedup_combine_pairs_identity_exact():
+    """Identity experts, unit weights, experts in pairs per peer: each
+    partial is 2x and y is k*x, both exact in bf16 (torch's casts)."""
+    import torch
+    for k in (2, 4, 8):
+        cfg = wl.custom(60, 136, 32, 8, k, expert="identity", seed=60 + k)
+        idx = _pair_routing(60, k, 32, 8, seed=61 + k)
+        w = np.ones((60, k), np.float32)
+        c = _dedup_chain(cfg, idx, w, True)
+        assert c["st_l"] == 0 and c["st_y"] == 0
+        xf = (c["inp"]["x"].astype(np.uint32) << 16).view(np.float32)
+        want_y = _torch_bf16_bits(xf * np.float32(k))
+        want_y[want_y == 0x8000] = 0
+        assert np.array_equal(c["y"], want_y)
+        want_p = _torch_bf16_bits(xf * np.float32(2))
+        want_p[want_p == 0x8000] = 0
+        for r in range(8):
+            a, b = c["d"]["tok_offset"][r], c["d"]["tok_offset"][r + 1]
+            assert np.array_equal(c["parts"][r], want_p[c["d"]["tok_src"][a:b] // k])
+
+
+def pin_dedup_combine_unit_weights_matches_torch():
+    """Identity experts, unit weights, any routing: partial_r = bf16(n_r x)
+    with n_r the token's expert count on peer r, y = bf16(sum_r partial_r)
+    (exact in float32 here), both cast by torch."""
+    cfg = wl.custom(120, 72, 24, 6, 5, expert="identity", seed=71)
+    inp0 = wl.make_inputs(cfg)
+    idx = wl.mask_slots(inp0["topk_idx"], 0.1, seed=72)
+    T, k = idx.shape
+    c = _dedup_chain(cfg, idx, np.ones((T, k), np.float32), True)
+    xf = (c["inp"]["x"].astype(np.uint32) << 16).view(np.float32)
+    L = 4
+    want_y = np.zeros((T, 72), np.float32)
+    for t in range(T):
+        ranks = [int(e) // L for e in idx[t] if e >= 0]
+        for r in dict.fromkeys(ranks):
+            pbits = _torch_bf16_bits(xf[t] * np.float32(ranks.count(r)))
+            row = c["d"]["tok_pos"][t * k + [int(e) // L if e >= 0 else -1
+                                             for e in idx[t]].index(r)]
+            got = c["parts"][r][row - c["d"]["tok_offset"][r]]
+            pb = pbits.copy()
+            pb[pb == 0x8000] = 0
+            assert np.array_equal(got, pb), (t, r)
+            want_y[t] += (pbits.astype(np.uint32) << 16).view(np.float32)
+    yb = _torch_bf16_bits(want_y)
+    yb[yb == 0x8000] = 0
+    assert np.array_equal(c["y"], yb)
+
+
+def pin_dedup_combine_scaled_bound():
+    """Scaled experts, softmax weights: partials within two bf16 roundings of
+    x * sum over the peer's slots of w_j s_e, and y within three of
+    x * sum_j w_j s_e (all terms share x's sign)."""
+    cfg = wl.custom(200, 136, 32, 8, 6, zipf_s=1.2, seed=81)
+    inp0 = wl.make_inputs(cfg)
+    idx, w = inp0["topk_idx"], inp0["topk_w"]
+    c = _dedup_chain(cfg, idx, w, False)
+    xf = _bf16_rows_to_f64(c["inp"]["x"])
+    s = (1.0 + 0.01 * idx.astype(np.float64)) * w.astype(np.float64)
+    ref = xf * s.sum(1, keepdims=True)
+    err = np.abs(_bf16_rows_to_f64(c["y"]) - ref)
+    assert np.all(err <= 1.01 * 3 * 2.0 ** -8 * np.abs(ref))
+    T, k = idx.shape
+    L = 4
+    for t in range(0, T, 7):
+        for j0 in range(k):
+            q = c["d"]["tok_pos"][t * k + j0]
+            if q < 0:
+                continue
+            r = int(idx[t, j0]) // L
+            sel = (idx[t] // L) == r
+            pref = xf[t] * s[t, sel].sum()
+            got = _bf16_rows_to_f64(c["parts"][r][q - c["d"]["tok_offset"][r]])
+            assert np.all(np.abs(got - pref) <= 1.01 * 2 * 2.0 ** -8 * np.abs(pref))
+
+
+def pin_dedup_capacity():
+    """A short deduplicated region: rows past it are not written (sentinel
+    kept), their slots are not expanded, and bit 4 is set on both sides."""
+    cfg = wl.custom(100, 64, 16, 4, 3, seed=91)
+    inp0 = wl.make_inputs(cfg)
+    idx = inp0["topk_idx"]
+    c = _dedup_chain(cfg, idx, inp0["topk_w"], True, dcap_delta=[0, -5, 0, 0])
+    assert c["st_d"] == 4 and c["st_e"] == 4
+    d, lay, k = c["d"], c["lay"], idx.shape[1]
+    assert c["dregs"][1].shape[0] == d["tok_count"][1] - 5
+    # slots whose pair row is past the short region keep the sentinel
+    L = 4
+    for s_ in range(idx.size):
+        t, j = divmod(s_, k)
+        if lay["pos"][s_] < 0 or int(idx[t, j]) // L != 1:
+            continue
+        q = [d["tok_pos"][t * k + jj] for jj in range(k)
+             if d["tok_pos"][t * k + jj] >= 0 and int(idx[t, jj]) // L == 1][0]
+        row = c["regs"][1][lay["pos"][s_] - lay["rank_offset"][1]]
+        if q - d["tok_offset"][1] >= c["dcap"][1]:
+            assert np.all(row == 0xA5)
+        else:
+            assert np.array_equal(row, _rows_u8(c["inp"]["x"])[t])
+
+
 ALL_PINS = [v for k_, v in sorted(globals().items()) if k_.startswith("pin_")]

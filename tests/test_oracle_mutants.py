@@ -65,6 +65,23 @@ MUTANTS = [
      "acc[(size_t)h] -= w * oracle_bf16_to_double(row[h]);"),
     ("combine_last_slot_dropped", "for (int32_t j = 0; j < k; ++j) {\n      int32_t p = pos[t * k + j];\n      if (p < 0) continue;\n      int32_t r = topk_idx[t * k + j] / L;\n      int64_t local = (int64_t)p - rank_offset[r];\n      if (local >= recv_cap[r]) { st |= kCapacity; continue; }\n      const uint16_t*",
      "for (int32_t j = 0; j + 1 < k; ++j) {\n      int32_t p = pos[t * k + j];\n      if (p < 0) continue;\n      int32_t r = topk_idx[t * k + j] / L;\n      int64_t local = (int64_t)p - rank_offset[r];\n      if (local >= recv_cap[r]) { st |= kCapacity; continue; }\n      const uint16_t*"),
+    ("dedup_pairs_by_expert", "if (used[(size_t)jj] && topk_idx[t * k + jj] / L == e / L) seen = true;",
+     "if (used[(size_t)jj] && topk_idx[t * k + jj] == e) seen = true;"),
+    ("dedup_counts_unused_slots", "if (used[(size_t)jj] && topk_idx[t * k + jj] / L == e / L) seen = true;",
+     "if (topk_idx[t * k + jj] / L == e / L) seen = true;"),
+    ("dedup_rows_reverse_token_order", "for (int64_t s = 0; s < S; ++s) {     // s = t*k + j ascending",
+     "for (int64_t s = S - 1; s >= 0; --s) {     // s = t*k + j ascending"),
+    ("dedup_offset_inclusive", "tok_offset[r + 1] = tok_offset[r] + tok_count[r];",
+     "tok_offset[r + 1] = tok_offset[r] + tok_count[r] + (r == 0);"),
+    ("expand_any_peer_row", "if (tok_pos[s] >= 0 && topk_idx[s] / L == r) return tok_pos[s];",
+     "if (tok_pos[s] >= 0) return tok_pos[s];"),
+    ("expand_scale_pad_kept", "std::memset(srow + scale_row_bytes, 0, (size_t)(scale_pitch - scale_row_bytes));",
+     ";"),
+    ("combine_local_all_peers", "if (p < 0 || topk_idx[t * k + j] / L != r) continue;",
+     "if (p < 0) continue;"),
+    ("combine_local_skips_first", "for (int32_t j = j0; j < k; ++j) {", "for (int32_t j = j0 + 1; j < k; ++j) {"),
+    ("combine_local_unweighted", "const double w = (double)topk_w[t * k + j];",
+     "const double w = 1.0;"),
     ("combine_no_capacity_flag", "if (local >= recv_cap[r]) { st |= kCapacity; continue; }\n      const uint16_t*",
      "if (local >= recv_cap[r]) { continue; }\n      const uint16_t*"),
 ]
