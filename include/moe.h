@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define MOE_VERSION 2
+#define MOE_VERSION 3
 
 #define MOE_OK 0
 #define MOE_EINVAL (-1)
@@ -268,6 +268,132 @@ int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int
                    const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
                    const void* workspace, size_t workspace_bytes, uint32_t* status,
                    int policy, int waves, uint64_t* trace, int trace_waves, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Per-peer deduplicated path.  A token with several experts on one rank is
+ * sent to that rank once: one row per routed (token, rank) pair ("pair
+ * row") instead of one per (token, expert) pair, so the bytes that cross to
+ * each peer -- the per-peer payload B_p that the partitioning of Section 6.2
+ * balances -- drop by the duplicates.  The receiving rank then rebuilds its
+ * expert windows locally (moe_expand) and, on the way back, reduces each
+ * pair's expert outputs to one partial row (moe_combine_local) that the
+ * source adds up (moe_combine_dedup).  Appendix D's first level (placement)
+ * and second level (expert windows) are unchanged; the peer windows of the
+ * third level hold pair rows.
+ *
+ * Pair rows of rank r are the global pair rows [tok_offset[r],
+ * tok_offset[r+1]), in token order, at region-local row (pair row -
+ * tok_offset[r]) of that rank's pair region.  A slot's pair is (t, e/L); the
+ * pair row is carried by the token's first routed slot on that rank.
+ * ------------------------------------------------------------------------ */
+
+/* Workspace bytes of moe_layout_dedup (written to *out_bytes, HOST).  Its
+ * front holds the pair-row plan: int32 bound[MOE_PLAN_PARTS + 1] over
+ * tokens, a token costing one row read plus one row per pair. */
+int moe_layout_dedup_workspace_bytes(int64_t T, int k, int E, int R, size_t* out_bytes);
+
+/*
+ * moe_layout_dedup -- placement of pair rows.  Slots are routed under the
+ * rules of moe_layout (unused, out-of-range and repeated experts are not;
+ * status bits 1 and 2 as there).
+ *
+ * Out: tok_count[R]       tokens sent to rank r (pairs of rank r);
+ *      tok_offset[R+1]    exclusive prefix sum of tok_count ([R] = pairs);
+ *      tok_pos[T*k]       on the first routed slot of token t on rank r:
+ *                         global pair row of (t, r) = tok_offset[r] +
+ *                         #{t' < t with a routed slot on r}; -1 on all other
+ *                         slots;
+ *      tok_src[T*k]       slot index t*k+j carrying each pair row (first
+ *                         tok_offset[R] entries; the rest are -1);
+ *      workspace          pair-row plan (see above) plus internal scratch,
+ *                         moe_layout_dedup_workspace_bytes, 256-byte aligned.
+ * A separate workspace from moe_layout's: the per-slot calls (moe_expand,
+ * moe_combine_local) read moe_layout's plan, the pair-row calls
+ * (moe_dispatch_dedup, moe_combine_dedup) read this one.
+ */
+int moe_layout_dedup(const int32_t* topk_idx, int64_t T, int k, int E, int R, int32_t* tok_count,
+                     int32_t* tok_offset, int32_t* tok_pos, int32_t* tok_src, void* workspace,
+                     size_t workspace_bytes, uint32_t* status, void* stream);
+
+/*
+ * moe_dispatch_dedup -- copy each pair row once: x[t] (and its fp8 scale
+ * row) to region r at local row tok_pos - tok_offset[r] for every slot with
+ * tok_pos >= 0 (Section 6.1 transfers, one per pair).  Arguments, layout,
+ * alignment and errors are those of moe_dispatch with (tok_pos, tok_offset)
+ * in place of (pos, rank_offset), regions sized in pair rows (recv_cap[r] >=
+ * tok_count[r] to keep every row) and the moe_layout_dedup workspace.
+ */
+int moe_dispatch_dedup(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,
+                       int E, int R, const int32_t* topk_idx, const int32_t* tok_pos,
+                       const int32_t* tok_offset, const uint64_t* recv_x,
+                       const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
+                       const void* workspace, size_t workspace_bytes, uint32_t* status,
+                       void* stream);
+
+/*
+ * moe_expand -- receiver side of the deduplicated dispatch: every routed
+ * slot (t, j) with expert e on rank r gets its pair row, copied from pair
+ * region r (local row pair row - tok_offset[r]) to expert-ordered region r
+ * at local row pos[t,j] - rank_offset[r].  The expert regions end up byte
+ * for byte as moe_dispatch leaves them (fp8 scale rows included, their
+ * pitch padding zeroed); each pair row is read once and written once per
+ * expert of the pair.
+ *
+ * dedup_x / dedup_scales / dedup_cap: pair regions as written by
+ *     moe_dispatch_dedup (scale rows scale_pitch bytes apart in both);
+ * recv_x / recv_scales / recv_cap: expert-ordered regions as for
+ *     moe_dispatch;
+ * pos, rank_offset, workspace: from moe_layout (its plan splits the work);
+ * tok_pos, tok_offset: from moe_layout_dedup.
+ * A pair row at or past dedup_cap[r], or a destination at or past
+ * recv_cap[r], is skipped and sets MOE_STATUS_CAPACITY.  Other errors as
+ * moe_dispatch.
+ */
+int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype, int64_t T,
+               int H, int k, int E, int R, const int32_t* topk_idx, const int32_t* pos,
+               const int32_t* rank_offset, const int32_t* tok_pos, const int32_t* tok_offset,
+               const int32_t* dedup_cap, const uint64_t* recv_x, const uint64_t* recv_scales,
+               int scale_pitch, const int32_t* recv_cap, const void* workspace,
+               size_t workspace_bytes, uint32_t* status, void* stream);
+
+/*
+ * moe_combine_local -- receiver side of the deduplicated combine: for every
+ * pair (t, r), the weighted sum of the token's expert outputs on rank r,
+ *      partial_r[q - tok_offset[r], :] = bf16( sum over routed slots j of
+ *                 token t with expert on r of topk_w[t,j] * Y_r[local, :] )
+ * (q the pair row; Y_r and local as in moe_combine; float32 products and
+ * sums, one rounding to bf16 to nearest-even).  Section 6.1 reduces on chip
+ * and writes once: each partial row has one writer.
+ *
+ * expert_y / recv_cap: bf16 expert-output regions (rows of 2H bytes);
+ * partial / part_cap: [R] bf16 partial regions in pair rows, 16-byte aligned;
+ * pos, rank_offset, workspace: from moe_layout; tok_pos, tok_offset: from
+ * moe_layout_dedup.  Expert rows at or past recv_cap[r] are not summed,
+ * pair rows at or past part_cap[r] are not written; both set
+ * MOE_STATUS_CAPACITY.  Other errors as moe_combine.
+ */
+int moe_combine_local(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
+                      int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                      const int32_t* rank_offset, const int32_t* recv_cap,
+                      const int32_t* tok_pos, const int32_t* tok_offset,
+                      const int32_t* part_cap, const uint64_t* partial, const void* workspace,
+                      size_t workspace_bytes, uint32_t* status, void* stream);
+
+/*
+ * moe_combine_dedup -- source side of the deduplicated combine:
+ *      y[t, :] = bf16( sum over the token's pairs (t, r) of
+ *                      partial_r[q - tok_offset[r], :] )
+ * in float32, rounded once to bf16 (nearest-even); a token with no pair gets
+ * +0.  Pair rows at or past part_cap[r] are skipped (MOE_STATUS_CAPACITY).
+ * Since each partial is itself rounded to bf16, y carries up to one more
+ * bf16 rounding per pair than moe_combine's result.  Workspace: from
+ * moe_layout_dedup.  Other arguments and errors as moe_combine.
+ */
+int moe_combine_dedup(const uint64_t* partial, int64_t T, int H, int k, int E, int R,
+                      const int32_t* topk_idx, const int32_t* tok_pos,
+                      const int32_t* tok_offset, const int32_t* part_cap, uint16_t* y,
+                      const void* workspace, size_t workspace_bytes, uint32_t* status,
+                      void* stream);
 
 /*
  * moe_expert_scale -- stand-in expert for tests and benchmarks, not part of

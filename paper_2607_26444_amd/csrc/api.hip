@@ -7,6 +7,7 @@
 #include <mutex>
 #include <utility>
 
+#include "dedup.h"
 #include "moe_internal.h"
 
 namespace moe {
@@ -135,13 +136,19 @@ int moe_layout_fixed(const int32_t* topk_idx, int64_t T, int k, int E, int R, in
                                      workspace, status, as_stream(stream)));
 }
 
-int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,
+}  // extern "C"
+
+namespace {
+
+// Shared by moe_dispatch_ex and moe_dispatch_dedup: plan and work tickets at
+// the front of a workspace of at least need_bytes.
+int dispatch_common(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,
                     int E, int R, const int32_t* topk_idx, const int32_t* pos,
                     const int32_t* rank_offset, const int32_t* row_src, const uint64_t* recv_x,
                     const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
-                    const void* workspace, size_t workspace_bytes, uint32_t* status,
-                    int policy, int waves, uint64_t* trace, int trace_waves,
-                    void* stream) {
+                    const void* workspace, size_t workspace_bytes, size_t need_bytes,
+                    size_t ticket_offset, uint32_t* status, int policy, int waves,
+                    uint64_t* trace, int trace_waves, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1 || (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3)) return MOE_EINVAL;
@@ -164,8 +171,7 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
   const int pitch = (fp8 && scale_pitch == 0) ? scale_row : scale_pitch;
   if (fp8 && (pitch < scale_row)) return MOE_EINVAL;
   if (fp8 && pitch % 4 != 0) return MOE_EALIGN;
-  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
-    return MOE_EWORKSPACE;
+  if (!aligned(workspace, 256) || workspace_bytes < need_bytes) return MOE_EWORKSPACE;
   if (T == 0) return MOE_OK;
   moe::DispatchArgs a;
   a.x = static_cast<const uint8_t*>(x);
@@ -186,11 +192,30 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
   a.row_src = row_src;
   a.R = R;
   a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
-                                          moe::layout_geom(T, E).ticket_offset);
+                                          ticket_offset);
   a.trace = trace;
   a.trace_waves = trace ? trace_waves : 0;
   a.launch_waves = waves;
   return launched(moe::launch_dispatch(a, policy, as_stream(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,
+                    int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                    const int32_t* rank_offset, const int32_t* row_src, const uint64_t* recv_x,
+                    const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
+                    const void* workspace, size_t workspace_bytes, uint32_t* status,
+                    int policy, int waves, uint64_t* trace, int trace_waves,
+                    void* stream) {
+  if (shape_ok(T, k, E, R)) return MOE_EINVAL;
+  const moe::LayoutGeom g = moe::layout_geom(T, E);
+  return dispatch_common(x, x_scales, dtype, T, H, k, E, R, topk_idx, pos, rank_offset, row_src,
+                         recv_x, recv_scales, scale_pitch, recv_cap, workspace, workspace_bytes,
+                         g.total, g.ticket_offset, status, policy, waves, trace, trace_waves,
+                         stream);
 }
 
 int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k, int E,
@@ -203,27 +228,31 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
                          status, MOE_POLICY_BALANCED, 0, nullptr, 0, stream);
 }
 
-int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
-                   int E, int R, const int32_t* topk_idx, const int32_t* pos,
+}  // extern "C"
+
+namespace {
+
+// Shared by moe_combine_ex and moe_combine_dedup (unit weights: topk_w null).
+int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weights, int64_t T,
+                   int H, int k, int E, int R, const int32_t* topk_idx, const int32_t* pos,
                    const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
-                   const void* workspace, size_t workspace_bytes, uint32_t* status,
-                   int policy, int waves, uint64_t* trace, int trace_waves,
-                   void* stream) {
+                   const void* workspace, size_t workspace_bytes, size_t need_bytes,
+                   size_t ticket_offset, uint32_t* status, int policy, int waves,
+                   uint64_t* trace, int trace_waves, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1) return MOE_EINVAL;
   if (!expert_y || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
-  if (T > 0 && (!topk_w || !topk_idx || !pos || !y)) return MOE_EINVAL;
+  if (T > 0 && ((!unit_weights && !topk_w) || !topk_idx || !pos || !y)) return MOE_EINVAL;
   if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_DYNAMIC) return MOE_EINVAL;
   if (!waves_ok(waves)) return MOE_EINVAL;
   if (trace && trace_waves < 0) return MOE_EINVAL;
   if ((2 * (int64_t)H) % 16 != 0 || !aligned(y, 16)) return MOE_EALIGN;
-  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
-    return MOE_EWORKSPACE;
+  if (!aligned(workspace, 256) || workspace_bytes < need_bytes) return MOE_EWORKSPACE;
   if (T == 0) return MOE_OK;
   moe::CombineArgs a;
   a.expert_y = expert_y;
-  a.topk_w = topk_w;
+  a.topk_w = unit_weights ? nullptr : topk_w;
   a.row_bytes = 2 * (int64_t)H;
   a.k = k;
   a.L = E / R;
@@ -238,8 +267,25 @@ int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int
   a.trace_waves = trace ? trace_waves : 0;
   a.launch_waves = waves;
   a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
-                                          moe::layout_geom(T, E).ticket_offset) + 2;
+                                          ticket_offset) + 2;
   return launched(moe::launch_combine(a, policy, as_stream(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
+                   int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                   const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
+                   const void* workspace, size_t workspace_bytes, uint32_t* status,
+                   int policy, int waves, uint64_t* trace, int trace_waves,
+                   void* stream) {
+  if (shape_ok(T, k, E, R)) return MOE_EINVAL;
+  const moe::LayoutGeom g = moe::layout_geom(T, E);
+  return combine_common(expert_y, topk_w, false, T, H, k, E, R, topk_idx, pos, rank_offset,
+                        recv_cap, y, workspace, workspace_bytes, g.total, g.ticket_offset,
+                        status, policy, waves, trace, trace_waves, stream);
 }
 
 int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k, int E,
@@ -282,6 +328,146 @@ int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int sc
   a.out_y = out_y;
   a.max_rows = max_rows;
   return launched(moe::launch_expert_scale(a, fp8, as_stream(stream)));
+}
+
+int moe_layout_dedup_workspace_bytes(int64_t T, int k, int E, int R, size_t* out_bytes) {
+  if (!out_bytes) return MOE_EINVAL;
+  const int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  *out_bytes = moe::dedup_geom(T, k, R).total;
+  return MOE_OK;
+}
+
+int moe_layout_dedup(const int32_t* topk_idx, int64_t T, int k, int E, int R, int32_t* tok_count,
+                     int32_t* tok_offset, int32_t* tok_pos, int32_t* tok_src, void* workspace,
+                     size_t workspace_bytes, uint32_t* status, void* stream) {
+  int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  if (!tok_count || !tok_offset || !workspace || !status) return MOE_EINVAL;
+  if (T > 0 && (!topk_idx || !tok_pos || !tok_src)) return MOE_EINVAL;
+  const moe::DedupGeom d = moe::dedup_geom(T, k, R);
+  if (!aligned(workspace, 256) || workspace_bytes < d.total) return MOE_EWORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  int32_t* rank_idx = reinterpret_cast<int32_t*>(ws + d.rank_idx_offset);
+  int32_t* spare = reinterpret_cast<int32_t*>(ws + d.spare_offset);
+  hipError_t err = hipSuccess;
+  if (T > 0) err = moe::launch_rank_index(topk_idx, T, k, E, E / R, rank_idx, status,
+                                          as_stream(stream));
+  if (err != hipSuccess) return launched(err);
+  // the layout pass over peers: one "expert" per peer, one peer per "rank"
+  return launched(moe::launch_layout(rank_idx, T, k, R, R, -1, tok_count, tok_offset, spare,
+                                     spare + R, tok_pos, tok_src, workspace, status,
+                                     as_stream(stream)));
+}
+
+int moe_dispatch_dedup(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,
+                       int E, int R, const int32_t* topk_idx, const int32_t* tok_pos,
+                       const int32_t* tok_offset, const uint64_t* recv_x,
+                       const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
+                       const void* workspace, size_t workspace_bytes, uint32_t* status,
+                       void* stream) {
+  if (shape_ok(T, k, E, R)) return MOE_EINVAL;
+  const moe::DedupGeom d = moe::dedup_geom(T, k, R);
+  return dispatch_common(x, x_scales, dtype, T, H, k, E, R, topk_idx, tok_pos, tok_offset,
+                         nullptr, recv_x, recv_scales, scale_pitch, recv_cap, workspace,
+                         workspace_bytes, d.total, d.g.ticket_offset, status,
+                         MOE_POLICY_BALANCED, 0, nullptr, 0, stream);
+}
+
+int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype, int64_t T,
+               int H, int k, int E, int R, const int32_t* topk_idx, const int32_t* pos,
+               const int32_t* rank_offset, const int32_t* tok_pos, const int32_t* tok_offset,
+               const int32_t* dedup_cap, const uint64_t* recv_x, const uint64_t* recv_scales,
+               int scale_pitch, const int32_t* recv_cap, const void* workspace,
+               size_t workspace_bytes, uint32_t* status, void* stream) {
+  int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  if (H < 1 || (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3)) return MOE_EINVAL;
+  const bool fp8 = dtype == MOE_DTYPE_FP8_E4M3;
+  if (!dedup_x || !dedup_cap || !recv_x || !recv_cap || !rank_offset || !tok_offset ||
+      !workspace || !status)
+    return MOE_EINVAL;
+  if (fp8 && (!dedup_scales || !recv_scales)) return MOE_EINVAL;
+  if (T > 0 && (!topk_idx || !pos || !tok_pos)) return MOE_EINVAL;
+  const int64_t row_bytes = fp8 ? (int64_t)H : 2 * (int64_t)H;
+  if (row_bytes % 16 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
+  const int scale_row = fp8 ? (H / MOE_FP8_BLOCK) * 4 : 0;
+  const int pitch = (fp8 && scale_pitch == 0) ? scale_row : scale_pitch;
+  if (fp8 && pitch < scale_row) return MOE_EINVAL;
+  if (fp8 && pitch % 4 != 0) return MOE_EALIGN;
+  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
+    return MOE_EWORKSPACE;
+  if (T == 0) return MOE_OK;
+  moe::ExpandArgs a;
+  a.dedup_x = dedup_x;
+  a.dedup_scales = fp8 ? dedup_scales : nullptr;
+  a.dedup_cap = dedup_cap;
+  a.recv_x = recv_x;
+  a.recv_scales = fp8 ? recv_scales : nullptr;
+  a.recv_cap = recv_cap;
+  a.row_bytes = row_bytes;
+  a.scale_row_bytes = scale_row;
+  a.scale_pitch = fp8 ? pitch : 0;
+  a.k = k;
+  a.L = E / R;
+  a.topk_idx = topk_idx;
+  a.pos = pos;
+  a.rank_offset = rank_offset;
+  a.tok_pos = tok_pos;
+  a.tok_offset = tok_offset;
+  a.bound = static_cast<const int32_t*>(workspace);
+  a.parts_per_wave = 0;
+  a.status = status;
+  return launched(moe::launch_expand(a, as_stream(stream)));
+}
+
+int moe_combine_local(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
+                      int E, int R, const int32_t* topk_idx, const int32_t* pos,
+                      const int32_t* rank_offset, const int32_t* recv_cap,
+                      const int32_t* tok_pos, const int32_t* tok_offset,
+                      const int32_t* part_cap, const uint64_t* partial, const void* workspace,
+                      size_t workspace_bytes, uint32_t* status, void* stream) {
+  int rc = shape_ok(T, k, E, R);
+  if (rc) return rc;
+  if (H < 1) return MOE_EINVAL;
+  if (!expert_y || !recv_cap || !rank_offset || !tok_offset || !part_cap || !partial ||
+      !workspace || !status)
+    return MOE_EINVAL;
+  if (T > 0 && (!topk_w || !topk_idx || !pos || !tok_pos)) return MOE_EINVAL;
+  if ((2 * (int64_t)H) % 16 != 0) return MOE_EALIGN;
+  if (!aligned(workspace, 256) || workspace_bytes < moe::layout_geom(T, E).total)
+    return MOE_EWORKSPACE;
+  if (T == 0) return MOE_OK;
+  moe::LocalArgs a;
+  a.expert_y = expert_y;
+  a.topk_w = topk_w;
+  a.recv_cap = recv_cap;
+  a.partial = partial;
+  a.part_cap = part_cap;
+  a.row_bytes = 2 * (int64_t)H;
+  a.k = k;
+  a.L = E / R;
+  a.topk_idx = topk_idx;
+  a.pos = pos;
+  a.rank_offset = rank_offset;
+  a.tok_pos = tok_pos;
+  a.tok_offset = tok_offset;
+  a.bound = static_cast<const int32_t*>(workspace);
+  a.parts_per_wave = 0;
+  a.status = status;
+  return launched(moe::launch_combine_local(a, as_stream(stream)));
+}
+
+int moe_combine_dedup(const uint64_t* partial, int64_t T, int H, int k, int E, int R,
+                      const int32_t* topk_idx, const int32_t* tok_pos,
+                      const int32_t* tok_offset, const int32_t* part_cap, uint16_t* y,
+                      const void* workspace, size_t workspace_bytes, uint32_t* status,
+                      void* stream) {
+  if (shape_ok(T, k, E, R)) return MOE_EINVAL;
+  const moe::DedupGeom d = moe::dedup_geom(T, k, R);
+  return combine_common(partial, nullptr, true, T, H, k, E, R, topk_idx, tok_pos, tok_offset,
+                        part_cap, y, workspace, workspace_bytes, d.total, d.g.ticket_offset,
+                        status, MOE_POLICY_BALANCED, 0, nullptr, 0, stream);
 }
 
 }  // extern "C"

@@ -138,7 +138,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
         const int local = p - a.rank_offset[r];
         if (local >= 0 && local < a.recv_cap[r]) {
           srow = a.expert_y[r] + (uint64_t)local * (uint64_t)rb;
-          wl = a.topk_w[s];
+          wl = a.topk_w ? a.topk_w[s] : 1.0f;   // null: unit weights
         } else {
           st |= MOE_STATUS_CAPACITY;
         }

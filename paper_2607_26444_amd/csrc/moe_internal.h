@@ -81,7 +81,7 @@ hipError_t launch_dispatch(const DispatchArgs& a, int policy, hipStream_t stream
 
 struct CombineArgs {
   const uint64_t* expert_y;
-  const float* topk_w;
+  const float* topk_w;         // nullptr: every weight is 1
   int64_t row_bytes;           // 2H
   int32_t k;
   int32_t L;

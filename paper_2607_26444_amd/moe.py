@@ -42,7 +42,9 @@ MOE_POLICY_DYNAMIC = 3
 # Entry points declared in include/moe.h.
 EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error", "moe_wall_clock_khz",
            "moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
-           "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale")
+           "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale",
+           "moe_layout_dedup_workspace_bytes", "moe_layout_dedup", "moe_dispatch_dedup",
+           "moe_expand", "moe_combine_local", "moe_combine_dedup")
 
 _lib = None
 P = ctypes.c_void_p
@@ -87,8 +89,19 @@ def lib() -> ctypes.CDLL:
         L.moe_combine_ex.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P,
                                      I32, I32, P, I32, P]
         L.moe_expert_scale.argtypes = [P, P, I32, I32, I32, I32, I32, I32, P, P, P, P, I64, P]
+        L.moe_layout_dedup_workspace_bytes.argtypes = [I64, I32, I32, I32, ctypes.POINTER(SZ)]
+        L.moe_layout_dedup.argtypes = [P, I64, I32, I32, I32, P, P, P, P, P, SZ, P, P]
+        L.moe_dispatch_dedup.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P,
+                                         I32, P, P, SZ, P, P]
+        L.moe_expand.argtypes = [P, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, P, P, P,
+                                 I32, P, P, SZ, P, P]
+        L.moe_combine_local.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, P, P,
+                                        P, SZ, P, P]
+        L.moe_combine_dedup.argtypes = [P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P, P]
         for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
-                  "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale"):
+                  "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale",
+                  "moe_layout_dedup_workspace_bytes", "moe_layout_dedup", "moe_dispatch_dedup",
+                  "moe_expand", "moe_combine_local", "moe_combine_dedup"):
             getattr(L, f).restype = I32
         _lib = L
     return _lib
@@ -197,6 +210,63 @@ def moe_expert_scale(recv_x, recv_scales, dtype, H, E, R, identity, expert_offse
         _stream(stream)))
 
 
+# ------------------------------------------------ per-peer deduplicated path
+def moe_layout_dedup_workspace_bytes(T: int, k: int, E: int, R: int) -> int:
+    out = SZ(0)
+    _check("moe_layout_dedup_workspace_bytes",
+           lib().moe_layout_dedup_workspace_bytes(T, k, E, R, ctypes.byref(out)))
+    return out.value
+
+
+def moe_layout_dedup(topk_idx, E, R, tok_count, tok_offset, tok_pos, tok_src, workspace,
+                     status, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_layout_dedup", lib().moe_layout_dedup(
+        _ptr(topk_idx), T, k, E, R, _ptr(tok_count), _ptr(tok_offset), _ptr(tok_pos),
+        _ptr(tok_src), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(status), _stream(stream)))
+
+
+def moe_dispatch_dedup(x, x_scales, dtype, H, E, R, topk_idx, tok_pos, tok_offset, recv_x,
+                       recv_scales, recv_cap, workspace, status, stream=None, scale_pitch=0):
+    T, k = topk_idx.shape
+    _check("moe_dispatch_dedup", lib().moe_dispatch_dedup(
+        _ptr(x), _ptr(x_scales), dtype, T, H, k, E, R, _ptr(topk_idx), _ptr(tok_pos),
+        _ptr(tok_offset), _ptr(recv_x), _ptr(recv_scales), scale_pitch, _ptr(recv_cap),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(status),
+        _stream(stream)))
+
+
+def moe_expand(dedup_x, dedup_scales, dtype, H, E, R, topk_idx, pos, rank_offset, tok_pos,
+               tok_offset, dedup_cap, recv_x, recv_scales, recv_cap, workspace, status,
+               stream=None, scale_pitch=0):
+    T, k = topk_idx.shape
+    _check("moe_expand", lib().moe_expand(
+        _ptr(dedup_x), _ptr(dedup_scales), dtype, T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
+        _ptr(rank_offset), _ptr(tok_pos), _ptr(tok_offset), _ptr(dedup_cap), _ptr(recv_x),
+        _ptr(recv_scales), scale_pitch, _ptr(recv_cap), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(status), _stream(stream)))
+
+
+def moe_combine_local(expert_y, topk_w, H, E, R, topk_idx, pos, rank_offset, recv_cap,
+                      tok_pos, tok_offset, part_cap, partial, workspace, status, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_combine_local", lib().moe_combine_local(
+        _ptr(expert_y), _ptr(topk_w), T, H, k, E, R, _ptr(topk_idx), _ptr(pos),
+        _ptr(rank_offset), _ptr(recv_cap), _ptr(tok_pos), _ptr(tok_offset), _ptr(part_cap),
+        _ptr(partial), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(status), _stream(stream)))
+
+
+def moe_combine_dedup(partial, H, E, R, topk_idx, tok_pos, tok_offset, part_cap, y, workspace,
+                      status, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_combine_dedup", lib().moe_combine_dedup(
+        _ptr(partial), T, H, k, E, R, _ptr(topk_idx), _ptr(tok_pos), _ptr(tok_offset),
+        _ptr(part_cap), _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(status), _stream(stream)))
+
+
 # ------------------------------------------------------------ buffer plumbing
 class Layout:
     """Device outputs of moe_layout (capacity None) or moe_layout_fixed
@@ -230,6 +300,29 @@ class Layout:
 
     def plan(self):
         """The partition plan bound[MOE_PLAN_PARTS + 1] (a view of the workspace)."""
+        return self.workspace[: (MOE_PLAN_PARTS + 1) * 4].view(torch.int32)
+
+
+class DedupLayout:
+    """Device outputs of moe_layout_dedup for one batch shape."""
+
+    def __init__(self, T, k, E, R, device="cuda"):
+        i32 = dict(dtype=torch.int32, device=device)
+        self.T, self.k, self.E, self.R = T, k, E, R
+        self.tok_count = torch.empty(R, **i32)
+        self.tok_offset = torch.empty(R + 1, **i32)
+        self.tok_pos = torch.empty(max(1, T * k), **i32)
+        self.tok_src = torch.empty(max(1, T * k), **i32)
+        nbytes = moe_layout_dedup_workspace_bytes(T, k, E, R)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        assert self.workspace.data_ptr() % 256 == 0
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def run(self, topk_idx, stream=None):
+        moe_layout_dedup(topk_idx, self.E, self.R, self.tok_count, self.tok_offset,
+                         self.tok_pos, self.tok_src, self.workspace, self.status, stream)
+
+    def plan(self):
         return self.workspace[: (MOE_PLAN_PARTS + 1) * 4].view(torch.int32)
 
 

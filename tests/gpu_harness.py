@@ -33,7 +33,7 @@ def to_dev(a: np.ndarray) -> torch.Tensor:
 
 def u8_rows(a: np.ndarray) -> np.ndarray:
     a = np.ascontiguousarray(a)
-    return a.view(np.uint8).reshape(a.shape[0], -1)
+    return a.view(np.uint8).reshape(a.shape[0], int(np.prod(a.shape[1:])) * a.itemsize)
 
 
 class GpuRun:
@@ -197,3 +197,113 @@ def f32_bits_to_bf16_rne(f32: np.ndarray) -> np.ndarray:
     """bf16 bit patterns of float32 values via torch's CPU cast (RNE)."""
     t = torch.from_numpy(np.ascontiguousarray(f32, np.float32)).to(torch.bfloat16)
     return t.view(torch.int16).numpy().view(np.uint16)
+
+
+class DedupRun:
+    """The per-peer deduplicated chain on the GPU: both layouts, dispatch of
+    pair rows, expansion into expert order, stand-in expert, partial combine
+    per pair and the source-side sum."""
+
+    def __init__(self, cfg, inp, topk_idx=None, topk_w=None, spare_rows=1, dcap_delta=None,
+                 pcap_delta=None, identity=None, scale_pitch=None):
+        T, H, E, R = cfg["T"], cfg["H"], cfg["E"], cfg["R"]
+        idx = inp["topk_idx"] if topk_idx is None else topk_idx
+        w = inp["topk_w"] if topk_w is None else topk_w
+        k = idx.shape[1]
+        fp8 = cfg["payload"] == wl.FP8_E4M3
+        dtype = moe.MOE_DTYPE_FP8_E4M3 if fp8 else moe.MOE_DTYPE_BF16
+        ident = (cfg["expert"] == "identity") if identity is None else identity
+        self.idx, self.w, self.k = idx, w, k
+        idx_d = to_dev(idx.astype(np.int32))
+        w_d = to_dev(w.astype(np.float32))
+        lay = moe.Layout(T, k, E, R)
+        lay.run(idx_d)
+        dl = moe.DedupLayout(T, k, E, R)
+        dl.run(idx_d)
+        torch.cuda.synchronize()
+
+        def caps(counts, delta):
+            c = counts.astype(np.int64) + spare_rows
+            if delta is not None:
+                c = np.maximum(0, c + np.asarray(delta))
+            return c.astype(np.int32)
+        self.caps = caps(lay.rank_count.cpu().numpy(), None)
+        self.dcaps = caps(dl.tok_count.cpu().numpy(), dcap_delta)
+        self.pcaps = caps(dl.tok_count.cpu().numpy(), pcap_delta)
+        rb, sb = wl.row_bytes(cfg), wl.scale_row_bytes(cfg)
+        self.scale_pitch = (sb + 127) // 128 * 128 if scale_pitch is None else (scale_pitch or sb)
+        sp = self.scale_pitch
+
+        def regions(rows, width):
+            return moe.Regions([int(c) for c in rows], width, guard_bytes=GUARD, fill=SENTINEL)
+        self.dregions = regions(self.dcaps, rb)
+        self.dsregions = regions(self.dcaps, sp) if fp8 else None
+        x_d = to_dev(u8_rows(inp["x"]))
+        xs_d = to_dev(inp["x_scales"]).view(torch.float32) if fp8 else None
+        self.st_dispatch = torch.zeros(1, dtype=torch.int32, device="cuda")
+        moe.moe_dispatch_dedup(x_d, xs_d, dtype, H, E, R, idx_d, dl.tok_pos, dl.tok_offset,
+                               self.dregions.table,
+                               self.dsregions.table if fp8 else None, self.dregions.cap,
+                               dl.workspace, self.st_dispatch, scale_pitch=sp)
+        self.regions = regions(self.caps, rb)
+        self.sregions = regions(self.caps, sp) if fp8 else None
+        self.st_expand = torch.zeros(1, dtype=torch.int32, device="cuda")
+        moe.moe_expand(self.dregions.table, self.dsregions.table if fp8 else None, dtype, H, E,
+                       R, idx_d, lay.pos, lay.rank_offset, dl.tok_pos, dl.tok_offset,
+                       self.dregions.cap, self.regions.table,
+                       self.sregions.table if fp8 else None, self.regions.cap, lay.workspace,
+                       self.st_expand, scale_pitch=sp)
+        self.eregions = regions(self.caps, 2 * H)
+        moe.moe_expert_scale(self.regions.table, self.sregions.table if fp8 else None, dtype, H,
+                             E, R, ident, lay.expert_offset, lay.rank_offset, self.regions.cap,
+                             self.eregions.table, max(1, T * k), scale_pitch=sp)
+        self.pregions = regions(self.pcaps, 2 * H)
+        self.st_local = torch.zeros(1, dtype=torch.int32, device="cuda")
+        moe.moe_combine_local(self.eregions.table, w_d, H, E, R, idx_d, lay.pos,
+                              lay.rank_offset, self.eregions.cap, dl.tok_pos, dl.tok_offset,
+                              self.pregions.cap, self.pregions.table, lay.workspace,
+                              self.st_local)
+        y = torch.empty((max(1, T), H), dtype=torch.int16, device="cuda")
+        y.fill_(0x5A5A)
+        self.st_sum = torch.zeros(1, dtype=torch.int32, device="cuda")
+        moe.moe_combine_dedup(self.pregions.table, H, E, R, idx_d, dl.tok_pos, dl.tok_offset,
+                              self.pregions.cap, y, dl.workspace, self.st_sum)
+        torch.cuda.synchronize()
+        self.dedup = dict(tok_count=dl.tok_count.cpu().numpy(),
+                          tok_offset=dl.tok_offset.cpu().numpy(),
+                          tok_pos=dl.tok_pos.cpu().numpy()[: T * k],
+                          tok_src=dl.tok_src.cpu().numpy()[: T * k],
+                          status=int(dl.status.cpu().numpy()[0]))
+        self.plan = dl.plan().cpu().numpy()
+        self.status = {n: int(getattr(self, "st_" + n).cpu().numpy()[0])
+                       for n in ("dispatch", "expand", "local", "sum")}
+        self.y = y.cpu().numpy().view(np.uint16)[:T]
+
+
+def oracle_dedup_chain(cfg, inp, run, topk_idx=None, topk_w=None, identity=None):
+    """The oracle's deduplicated chain on the same inputs and region sizes."""
+    E, R, H = cfg["E"], cfg["R"], cfg["H"]
+    idx = inp["topk_idx"] if topk_idx is None else topk_idx
+    w = inp["topk_w"] if topk_w is None else topk_w
+    fp8 = cfg["payload"] == wl.FP8_E4M3
+    ident = (cfg["expert"] == "identity") if identity is None else identity
+    lay = oracle.layout(idx, E, R)
+    d = oracle.layout_dedup(idx, E, R)
+    xs = u8_rows(inp["x_scales"]) if fp8 else None
+    dregs, dsregs, st_d = oracle.dispatch_dedup(u8_rows(inp["x"]), xs, idx, d["tok_pos"],
+                                                d["tok_offset"], E, R, run.dcaps, SENTINEL,
+                                                scale_pitch=run.scale_pitch if fp8 else 0)
+    srb = xs.shape[1] if fp8 else 0
+    regs, sregs, st_e = oracle.expand(dregs, dsregs, srb, idx, lay["pos"], lay["rank_offset"],
+                                      d["tok_pos"], d["tok_offset"], run.dcaps, E, R, run.caps,
+                                      SENTINEL)
+    ey = oracle.expert_scale(regs, sregs, fp8, H, E, R, ident, lay["expert_offset"],
+                             lay["rank_offset"], run.caps)
+    parts, st_l = oracle.combine_local(ey, w, idx, lay["pos"], lay["rank_offset"], run.caps,
+                                       d["tok_pos"], d["tok_offset"], run.pcaps, E, R, H,
+                                       sentinel=SENTINEL * 0x101)
+    y, st_y = oracle.combine_dedup(parts, idx, d["tok_pos"], d["tok_offset"], run.pcaps, E, R,
+                                   H)
+    return dict(layout=lay, dedup=d, dregs=dregs, dsregs=dsregs, regs=regs, sregs=sregs,
+                ey=ey, parts=parts, y=y,
+                status=dict(dispatch=st_d, expand=st_e, local=st_l, sum=st_y))

@@ -39,7 +39,7 @@ def test_binding_covers_every_declared_symbol():
 
 
 def test_version_and_strerror():
-    assert moe.moe_version() == 2
+    assert moe.moe_version() == 3
     for code in (0, -1, -2, -3, -4, -99):
         assert isinstance(moe.lib().moe_strerror(code), bytes)
 
@@ -138,3 +138,56 @@ def test_no_fallback_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(moe, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="no fallback"):
         moe.lib()
+
+
+def test_dedup_argument_errors():
+    L = moe.lib()
+    n = moe.moe_layout_dedup_workspace_bytes(64, 8, 256, 64)
+    n_slot = moe.moe_layout_workspace_bytes(64, 8, 256, 64)
+    assert n >= (moe.MOE_PLAN_PARTS + 1) * 4 + 64 * 8 * 4
+    out = ctypes.c_size_t(0)
+    assert L.moe_layout_dedup_workspace_bytes(16, 8, 256, 60, ctypes.byref(out)) == moe.MOE_EINVAL
+    # layout
+    ok = [FAKE, 64, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, WS, n, FAKE, None]
+    assert L.moe_layout_dedup(*ok[:10], n - 4, *ok[11:]) == moe.MOE_EWORKSPACE
+    bad = list(ok); bad[5] = None
+    assert L.moe_layout_dedup(*bad) == moe.MOE_EINVAL
+    bad = list(ok); bad[9] = ctypes.c_void_p(0x100010)
+    assert L.moe_layout_dedup(*bad) == moe.MOE_EWORKSPACE
+    # dispatch of pair rows: the pair-row workspace size is required
+    d = [FAKE, None, 0, 64, 7168, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, None, 0, FAKE, WS, n,
+         FAKE, None]
+    bad = list(d); bad[16] = min(n, n_slot) - 4
+    assert L.moe_dispatch_dedup(*bad) == moe.MOE_EWORKSPACE
+    bad = list(d); bad[0] = MIS
+    assert L.moe_dispatch_dedup(*bad) == moe.MOE_EALIGN
+    bad = list(d); bad[2] = 5
+    assert L.moe_dispatch_dedup(*bad) == moe.MOE_EINVAL
+    # expand
+    e = [FAKE, None, 0, 64, 7168, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0,
+         FAKE, WS, n_slot, FAKE, None]
+    bad = list(e); bad[13] = None                      # dedup_cap
+    assert L.moe_expand(*bad) == moe.MOE_EINVAL
+    bad = list(e); bad[2] = 1                          # fp8 without scale regions
+    assert L.moe_expand(*bad) == moe.MOE_EINVAL
+    bad = list(e); bad[4] = 7164
+    assert L.moe_expand(*bad) == moe.MOE_EALIGN
+    bad = list(e); bad[19] = 8
+    assert L.moe_expand(*bad) == moe.MOE_EWORKSPACE
+    # partial combine
+    c = [FAKE, FAKE, 64, 7168, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, WS,
+         n_slot, FAKE, None]
+    bad = list(c); bad[14] = None                      # partial table
+    assert L.moe_combine_local(*bad) == moe.MOE_EINVAL
+    bad = list(c); bad[1] = None                       # weights
+    assert L.moe_combine_local(*bad) == moe.MOE_EINVAL
+    bad = list(c); bad[16] = 16
+    assert L.moe_combine_local(*bad) == moe.MOE_EWORKSPACE
+    # source-side sum
+    s = [FAKE, 64, 7168, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, WS, n, FAKE, None]
+    bad = list(s); bad[10] = MIS                       # y
+    assert L.moe_combine_dedup(*bad) == moe.MOE_EALIGN
+    bad = list(s); bad[12] = n - 4
+    assert L.moe_combine_dedup(*bad) == moe.MOE_EWORKSPACE
+    bad = list(s); bad[0] = None
+    assert L.moe_combine_dedup(*bad) == moe.MOE_EINVAL

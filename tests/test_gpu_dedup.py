@@ -1,0 +1,144 @@
+"""Per-peer deduplicated path on the GPU against the oracle.
+
+Pair-row layout, its plan, the pair regions, the expanded expert regions and
+every status word are compared exactly.  Partial rows and y are bf16 sums
+computed in float32 on the GPU and in double in the oracle: partials within
+8e-3*|ref| + 1e-3 (one rounding of a float32 sum, as for moe_combine), y
+within 1.6e-2*|ref| + 1e-3 -- a partial that lands on the other side of a
+rounding boundary moves by up to 2^-7 of itself, and with the stand-in
+experts' positive scales and the positive softmax weights every partial of
+a token has y's sign, so those moves add up to at most 2^-7 |y| on top of
+the 2^-7 |y| of y's own rounding.
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from paper_2607_26444_amd import moe
+
+pytestmark = pytest.mark.gpu
+
+
+def _h():
+    import gpu_harness
+    return gpu_harness
+
+
+def _close(h, got_u16, want_u16, rtol, what):
+    ok, msg = h.combine_close(got_u16, want_u16, rtol=rtol)
+    assert ok, f"{what}: {msg}"
+
+
+def _dedup_parity(cfg, inp=None, idx=None, w=None, **kw):
+    h = _h()
+    inp = wl.make_inputs(cfg) if inp is None else inp
+    idx = inp["topk_idx"] if idx is None else idx
+    h.log(f"[dedup] {cfg['name']} T={cfg['T']} H={cfg['H']} E={cfg['E']} R={cfg['R']} "
+          f"k={idx.shape[1]} {kw}")
+    run = h.DedupRun(cfg, inp, topk_idx=idx, topk_w=w, **kw)
+    ref = h.oracle_dedup_chain(cfg, inp, run, topk_idx=idx, topk_w=w)
+    T, k = idx.shape
+    for key in ("tok_count", "tok_offset", "tok_pos", "tok_src", "status"):
+        assert np.array_equal(np.asarray(run.dedup[key]), np.asarray(ref["dedup"][key])), key
+    assert np.array_equal(run.plan, oracle_plan(ref["dedup"]["tok_pos"], T, k)), "plan"
+    assert run.status == ref["status"], (run.status, ref["status"])
+    h.check_regions(None, run.dregions, ref["dregs"])
+    if run.dsregions is not None:
+        h.check_regions(None, run.dsregions, ref["dsregs"])
+    h.check_regions(None, run.regions, ref["regs"])
+    if run.sregions is not None:
+        h.check_regions(None, run.sregions, ref["sregs"])
+    # partial rows: written rows within tolerance, the rest keep the sentinel
+    buf = run.pregions.buf.cpu().numpy()
+    H = cfg["H"]
+    for r, off in enumerate(run.pregions.offsets):
+        n_cap = run.pregions.rows[r]
+        got = buf[off: off + n_cap * 2 * H].view(np.uint16).reshape(n_cap, H)
+        want = ref["parts"][r]
+        n = min(int(ref["dedup"]["tok_count"][r]), n_cap)
+        assert np.all(got[n:] == h.SENTINEL * 0x101), f"partial region {r}: rows past {n}"
+        _close(h, got[:n], want[:n], 8e-3, f"partial region {r}")
+    _close(h, run.y, ref["y"], 1.6e-2, "y")
+    return run, ref
+
+
+def oracle_plan(tok_pos, T, k):
+    import oracle
+    return oracle.plan(tok_pos, T, k, moe.MOE_PLAN_PARTS)
+
+
+@pytest.mark.parametrize("T,H,E,R,k,payload,mask,zipf", [
+    (1000, 1032, 24, 6, 3, wl.BF16, 0.1, 0.0),
+    (700, 640, 32, 8, 5, wl.FP8_E4M3, 0.05, 0.0),
+    (2049, 7168, 256, 64, 8, wl.BF16, 0.0, 1.2),
+    (513, 4096, 128, 32, 8, wl.FP8_E4M3, 0.0, 1.2),
+    (300, 256, 16, 4, 1, wl.BF16, 0.0, 0.0),       # k = 1: every slot is a pair
+    (200, 512, 16, 16, 4, wl.BF16, 0.0, 0.0),      # one expert per peer
+    (150, 256, 8, 1, 4, wl.BF16, 0.0, 0.0),        # one peer
+    (300, 256, 8, 2, 6, wl.BF16, 0.1, 0.0),        # k > R: many slots per pair
+    (257, 2048, 64, 8, 16, wl.BF16, 0.0, 1.2),
+    (100, 512, 64, 8, 32, wl.BF16, 0.05, 0.0),     # 32 slots
+    (333, 1024, 48, 12, 7, wl.FP8_E4M3, 0.0, 0.0), # scale rows of 32 bytes
+])
+def test_dedup_chain_matches_oracle(T, H, E, R, k, payload, mask, zipf):
+    cfg = wl.custom(T, H, E, R, k, payload=payload, zipf_s=zipf, seed=T + 7)
+    inp = wl.make_inputs(cfg)
+    idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
+    _dedup_parity(cfg, inp, idx=idx)
+
+
+def test_dedup_expand_rebuilds_per_slot_dispatch():
+    """The expanded expert regions are the per-slot dispatch's, byte for byte
+    (run both on the GPU; each is also checked against the oracle)."""
+    h = _h()
+    cfg = wl.custom(900, 2048, 64, 16, 6, zipf_s=1.2, seed=5)
+    inp = wl.make_inputs(cfg)
+    run, _ = _dedup_parity(cfg, inp)
+    ref = h.GpuRun(cfg, inp, spare_rows=1)
+    a = run.regions.buf.cpu().numpy()
+    b = ref.regions.buf.cpu().numpy()
+    for r in range(cfg["R"]):
+        n = run.regions.rows[r] * run.regions.row_bytes
+        assert np.array_equal(a[run.regions.offsets[r]: run.regions.offsets[r] + n],
+                              b[ref.regions.offsets[r]: ref.regions.offsets[r] + n]), r
+
+
+def test_dedup_capacity_overflow():
+    """Short pair and partial regions: rows past them are neither written
+    nor read, every stage flags bit 4, and the oracle agrees row by row."""
+    cfg = wl.custom(800, 1024, 32, 8, 6, zipf_s=1.2, seed=3)
+    dd = [0] * 8
+    dd[0] = -40
+    pd = [0] * 8
+    pd[2] = -7
+    run, ref = _dedup_parity(cfg, spare_rows=0, dcap_delta=dd, pcap_delta=pd)
+    assert run.status["dispatch"] == moe.MOE_STATUS_CAPACITY
+    assert run.status["expand"] == moe.MOE_STATUS_CAPACITY
+    assert run.status["local"] == moe.MOE_STATUS_CAPACITY
+
+
+def test_dedup_bad_and_repeated_indices():
+    cfg = wl.custom(400, 512, 32, 8, 5, seed=11)
+    inp = wl.make_inputs(cfg)
+    idx = inp["topk_idx"].copy()
+    idx[3, 1] = 32          # out of range
+    idx[5, 2] = -7          # out of range (negative)
+    idx[7, 4] = idx[7, 0]   # repeat
+    idx[9, :] = -1          # token with no routed slot
+    run, _ = _dedup_parity(cfg, inp, idx=idx)
+    assert run.dedup["status"] == moe.MOE_STATUS_BAD_INDEX | moe.MOE_STATUS_DUP_INDEX
+    assert np.all(run.y[9] == 0)
+
+
+def test_dedup_zero_tokens():
+    cfg = wl.custom(0, 256, 16, 4, 2, seed=1)
+    _dedup_parity(cfg)
+
+
+@pytest.mark.parametrize("name", ["decode", "prefill"])
+def test_dedup_full_size(name):
+    cfg = wl.get(name)
+    run, ref = _dedup_parity(cfg)
+    n_pairs = int(ref["dedup"]["tok_offset"][-1])
+    _h().log(f"[dedup] {name}: {n_pairs} pair rows for {cfg['T'] * cfg['k']} slots "
+             f"({n_pairs / (cfg['T'] * cfg['k']):.3f})")
