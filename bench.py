@@ -244,6 +244,125 @@ def ablation(a):
     return 0 if st == 0 else 1
 
 
+def dedup_bench(a):
+    """The per-peer deduplicated path on one workload: per-kernel time (HIP
+    events on the launch stream) and GB/s of each kernel's algorithmic
+    bytes, the pair-row fraction (bytes that would cross to peers, relative
+    to one row per routed slot) and the per-slot step beside it.  One JSON
+    line."""
+    import torch
+    import workloads as wl
+    from paper_2607_26444_amd import moe
+
+    cfg = wl.get(a.workload)
+    T, H, E, R, k = cfg["T"], cfg["H"], cfg["E"], cfg["R"], cfg["k"]
+    fp8 = cfg["payload"] == wl.FP8_E4M3
+    dtype = moe.MOE_DTYPE_FP8_E4M3 if fp8 else moe.MOE_DTYPE_BF16
+    print(f"[dedup] workload {cfg['name']}: generating inputs", file=sys.stderr, flush=True)
+    inp = wl.make_inputs(cfg)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    x_d = torch.from_numpy(np.ascontiguousarray(inp["x"]).view(np.uint8)).to(dev)
+    xs_d = torch.from_numpy(inp["x_scales"]).to(dev) if fp8 else None
+    idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
+    w_d = torch.from_numpy(inp["topk_w"]).to(dev)
+    lay = moe.Layout(T, k, E, R)
+    dl = moe.DedupLayout(T, k, E, R)
+    lay.run(idx_d)
+    dl.run(idx_d)
+    torch.cuda.synchronize()
+    rows = [max(1, int(c)) for c in lay.rank_count.cpu().numpy()]
+    prow = [max(1, int(c)) for c in dl.tok_count.cpu().numpy()]
+    n_slots, n_pairs = int(lay.rank_offset[-1].item()), int(dl.tok_offset[-1].item())
+    rb, sb = wl.row_bytes(cfg), wl.scale_row_bytes(cfg)
+    spitch = (sb + 127) // 128 * 128
+    dreg = moe.Regions(prow, rb)
+    dsreg = moe.Regions(prow, spitch) if fp8 else None
+    reg = moe.Regions(rows, rb)
+    sreg = moe.Regions(rows, spitch) if fp8 else None
+    ereg = moe.Regions(rows, 2 * H)
+    preg = moe.Regions(prow, 2 * H)
+    y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    ops = {
+        "layout": lambda: lay.run(idx_d),
+        "layout_dedup": lambda: dl.run(idx_d),
+        "dispatch_dedup": lambda: moe.moe_dispatch_dedup(
+            x_d, xs_d, dtype, H, E, R, idx_d, dl.tok_pos, dl.tok_offset, dreg.table,
+            dsreg.table if fp8 else None, dreg.cap, dl.workspace, status, scale_pitch=spitch),
+        "expand": lambda: moe.moe_expand(
+            dreg.table, dsreg.table if fp8 else None, dtype, H, E, R, idx_d, lay.pos,
+            lay.rank_offset, dl.tok_pos, dl.tok_offset, dreg.cap, reg.table,
+            sreg.table if fp8 else None, reg.cap, lay.workspace, status, scale_pitch=spitch),
+        "combine_local": lambda: moe.moe_combine_local(
+            ereg.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, ereg.cap, dl.tok_pos,
+            dl.tok_offset, preg.cap, preg.table, lay.workspace, status),
+        "combine_dedup": lambda: moe.moe_combine_dedup(
+            preg.table, H, E, R, idx_d, dl.tok_pos, dl.tok_offset, preg.cap, y, dl.workspace,
+            status),
+        "dispatch": lambda: moe.moe_dispatch(
+            x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset, reg.table,
+            sreg.table if fp8 else None, reg.cap, lay.workspace, status, scale_pitch=spitch),
+        "combine": lambda: moe.moe_combine(
+            ereg.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, ereg.cap, y,
+            lay.workspace, status),
+    }
+    ops["dispatch"]()
+    moe.moe_expert_scale(reg.table, sreg.table if fp8 else None, dtype, H, E, R,
+                         cfg["expert"] == "identity", lay.expert_offset, lay.rank_offset,
+                         reg.cap, ereg.table, sum(rows), scale_pitch=spitch)
+    torch.cuda.synchronize()
+    names = list(ops)
+    for _ in range(a.warmup):
+        for n in names:
+            ops[n]()
+    torch.cuda.synchronize()
+    ev = {n: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(a.steps)] for n in names}
+    for s_ in range(a.steps):
+        for n in names:
+            ev[n][s_][0].record(stream)
+            ops[n]()
+            ev[n][s_][1].record(stream)
+    torch.cuda.synchronize()
+    st = int(status.item()) | int(lay.status.item()) | int(dl.status.item())
+    us = {n: float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev[n]])) * 1e3 for n in names}
+    row = rb + sb                        # a row and its scales (fp8)
+    alg = {
+        "dispatch_dedup": T * row + n_pairs * row + 4 * T * k,
+        "expand": n_pairs * row + n_slots * row + 8 * T * k,
+        "combine_local": n_slots * 2 * H + n_pairs * 2 * H + 12 * T * k,
+        "combine_dedup": n_pairs * 2 * H + T * 2 * H + 4 * T * k,
+        "dispatch": T * row + n_slots * row + 4 * T * k,
+        "combine": n_slots * 2 * H + T * 2 * H + 8 * T * k,
+    }
+    kern = {n: {"us": round(us[n], 2)} for n in names}
+    for n, b in alg.items():
+        kern[n].update(bytes=int(b), GBps=round(b / (us[n] * 1e-6) / 1e9, 1),
+                       frac=round(b / (us[n] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4))
+    dedup_step = sum(us[n] for n in ("layout", "layout_dedup", "dispatch_dedup", "expand",
+                                     "combine_local", "combine_dedup"))
+    slot_step = sum(us[n] for n in ("layout", "dispatch", "combine"))
+    out = {
+        "metric": "per-peer deduplicated dispatch/combine: per-kernel HBM GB/s",
+        "config": {"workload": cfg["name"], "T": T, "H": H, "E": E, "R": R, "k": k,
+                   "payload": "fp8_e4m3" if fp8 else "bf16"},
+        "steps": a.steps, "warmup": a.warmup,
+        "slots": n_slots, "pair_rows": n_pairs,
+        "pair_row_fraction": round(n_pairs / max(1, n_slots), 4),
+        "peer_bytes_dispatch": {"per_slot": n_slots * row, "dedup": n_pairs * row},
+        "peer_bytes_combine": {"per_slot": n_slots * 2 * H, "dedup": n_pairs * 2 * H},
+        "kernels": kern,
+        "dedup_step_us": round(dedup_step, 2),
+        "per_slot_step_us": round(slot_step, 2),
+        "status": st,
+    }
+    print(json.dumps(out), flush=True)
+    return 0 if st == 0 else 1
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -257,16 +376,20 @@ def main(argv=None):
                     help="fixed-capacity layout with windows of F x the mean expert load")
     ap.add_argument("--cold-reps", type=int, default=20,
                     help="repetitions of the cold-cache pass (0 skips it)")
+    ap.add_argument("--dedup", action="store_true",
+                    help="instead of the step benchmark: the per-peer deduplicated path")
     ap.add_argument("--graph", action="store_true",
                     help="capture each step in a graph (needs --ll: no host sync in a step)")
     a = ap.parse_args(argv)
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the operator; runs on more than "
-              "one GPU are not part of this build (use --gpus 1).", file=sys.stderr)
+              "one GPU are not supported (use --gpus 1).", file=sys.stderr)
         return 2
 
     if a.ablation:
         return ablation(a)
+    if a.dedup:
+        return dedup_bench(a)
 
     import torch
     import workloads as wl
