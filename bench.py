@@ -87,7 +87,7 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(cfg, inp, budget_s=12.0, max_reps=3):
+def cpu_baseline(cfg, inp, budget_s=20.0, max_reps=5):
     """The CPU oracle (single-threaded) on the same workload: layout, dispatch
     and combine, timed on this host.  Its combine reads the dispatched rows
     directly (identity expert); the cost does not depend on the values."""
