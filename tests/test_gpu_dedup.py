@@ -79,6 +79,10 @@ def oracle_plan(tok_pos, T, k):
     (257, 2048, 64, 8, 16, wl.BF16, 0.0, 1.2),
     (100, 512, 64, 8, 32, wl.BF16, 0.05, 0.0),     # 32 slots
     (333, 1024, 48, 12, 7, wl.FP8_E4M3, 0.0, 0.0), # scale rows of 32 bytes
+    (2000, 256, 1024, 64, 8, wl.BF16, 0.05, 1.2),  # MOE_MAX_EXPERTS
+    (300, 16384, 64, 8, 4, wl.BF16, 0.0, 0.0),     # 32 KiB rows: two passes
+    (100, 20480, 32, 8, 2, wl.FP8_E4M3, 0.0, 0.0), # 640-byte scale rows
+    (131072, 128, 256, 64, 8, wl.BF16, 0.0, 1.2),  # 1M slots
 ])
 def test_dedup_chain_matches_oracle(T, H, E, R, k, payload, mask, zipf):
     cfg = wl.custom(T, H, E, R, k, payload=payload, zipf_s=zipf, seed=T + 7)

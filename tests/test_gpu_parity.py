@@ -105,6 +105,10 @@ def test_tiny_identity_softmax_returns_x():
     (256, 512, 32, 8, 4, wl.BF16, 0.1),        # largest single-kernel layout
     (257, 512, 32, 8, 4, wl.BF16, 0.1),        # smallest two-kernel layout
     (300, 2048, 16, 4, 2, wl.FP8_E4M3, 0.0),   # 64-byte scale rows
+    (2000, 256, 1024, 64, 8, wl.BF16, 0.05),   # MOE_MAX_EXPERTS
+    (300, 16384, 64, 8, 4, wl.BF16, 0.0),      # 32 KiB rows: two 16 KiB passes
+    (100, 20480, 32, 8, 2, wl.FP8_E4M3, 0.0),  # 20 KiB fp8 rows, 640-byte scale rows
+    (131072, 128, 256, 64, 8, wl.BF16, 0.0),   # 1M slots, 128 layout chunks
     (90, 8192, 64, 16, 6, wl.FP8_E4M3, 0.1),   # 256-byte scale rows, k=6
     (64, 1152, 1024, 256, 8, wl.BF16, 0.0),    # maximum expert count
 ])
