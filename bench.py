@@ -366,7 +366,8 @@ def dedup_bench(a):
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 100; 1000 for the tiny workload)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="prefill")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -381,6 +382,8 @@ def main(argv=None):
     ap.add_argument("--graph", action="store_true",
                     help="capture each step in a graph (needs --ll: no host sync in a step)")
     a = ap.parse_args(argv)
+    if a.steps is None:
+        a.steps = 1000 if a.workload in ("tiny", "tiny_t128_h256_e16_r4_k2") else 100
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the operator; runs on more than "
               "one GPU are not supported (use --gpus 1).", file=sys.stderr)
@@ -598,6 +601,20 @@ def main(argv=None):
     torch.cuda.synchronize()
     out["hbm_copy_GBps"] = round(2 * src.numel() * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
     del src, dst
+    # ... and a copy that moves as many bytes as dispatch + combine
+    half = max(16, dc_bytes // 2 // 16 * 16)
+    src = torch.empty(half, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    out["hbm_copy_equal_bytes_GBps"] = round(2 * half * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9,
+                                             1)
+    del src, dst
 
     if not a.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
@@ -607,7 +624,7 @@ def main(argv=None):
             "kind": "oracle",
             "sample": f"full workload (layout+dispatch+combine), median of {reps} run(s), "
                       f"{cpu_s:.2f} s each, 1 thread, host CPU: {cpu_model()}",
-            "tokens_per_s": round(T / cpu_s, 1)}
+            "tokens_per_s": round(T / cpu_s, 1), "host_nproc": os.cpu_count()}
     print(json.dumps(out), flush=True)
     return 0
 
