@@ -87,10 +87,11 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(cfg, inp, budget_s=20.0, max_reps=5):
-    """The CPU oracle (single-threaded) on the same workload: layout, dispatch
-    and combine, timed on this host.  Its combine reads the dispatched rows
-    directly (identity expert); the cost does not depend on the values."""
+def cpu_baseline(cfg, inp, budget_s=20.0, max_reps=5, capacity=None):
+    """The CPU oracle (single-threaded) on the same workload: layout (the
+    fixed-capacity one when `capacity` is set), dispatch and combine, timed
+    on this host.  Its combine reads the dispatched rows directly (identity
+    expert); the cost does not depend on the values."""
     import oracle
     E, R, H = cfg["E"], cfg["R"], cfg["H"]
     fp8 = cfg["payload"] == 1
@@ -101,10 +102,15 @@ def cpu_baseline(cfg, inp, budget_s=20.0, max_reps=5):
     t_start = time.perf_counter()
     for _ in range(max_reps):
         t0 = time.perf_counter()
-        lay = oracle.layout(inp["topk_idx"], E, R)
+        if capacity is None:
+            lay = oracle.layout(inp["topk_idx"], E, R)
+            caps = lay["rank_count"]
+        else:
+            lay = oracle.layout_fixed(inp["topk_idx"], E, R, capacity)
+            caps = np.full(R, (E // R) * capacity, np.int32)
         t1 = time.perf_counter()
         regs, _, _ = oracle.dispatch(x_rows, xs_rows, inp["topk_idx"], lay["pos"],
-                                     lay["rank_offset"], E, R, lay["rank_count"])
+                                     lay["rank_offset"], E, R, caps)
         t2 = time.perf_counter()
         if fp8:
             ey = [np.zeros((r.shape[0], H), np.uint16) for r in regs]
@@ -112,10 +118,55 @@ def cpu_baseline(cfg, inp, budget_s=20.0, max_reps=5):
             ey = [r.view(np.uint16).reshape(r.shape[0], H) for r in regs]
         t3 = time.perf_counter()
         oracle.combine(ey, inp["topk_w"], inp["topk_idx"], lay["pos"], lay["rank_offset"],
-                       lay["rank_count"], E, R, H)
+                       caps, E, R, H)
         t4 = time.perf_counter()
         times.append((t1 - t0) + (t2 - t1) + (t4 - t3))
         del regs, ey
+        if time.perf_counter() - t_start > budget_s:
+            break
+    return float(np.median(times)), len(times)
+
+
+def cpu_baseline_dedup(cfg, inp, n_tokens, budget_s=20.0, max_reps=5):
+    """The CPU oracle's deduplicated chain on the first n_tokens tokens of
+    the workload (both layouts, pair dispatch, expansion, partial combine,
+    source sum; the expanded rows stand in for expert outputs), timed on
+    this host."""
+    import oracle
+    E, R, H = cfg["E"], cfg["R"], cfg["H"]
+    fp8 = cfg["payload"] == 1
+    n = n_tokens
+    idx = np.ascontiguousarray(inp["topk_idx"][:n])
+    x_rows = np.ascontiguousarray(inp["x"][:n]).view(np.uint8).reshape(n, -1)
+    xs_rows = (np.ascontiguousarray(inp["x_scales"][:n]).view(np.uint8).reshape(n, -1)
+               if fp8 else None)
+    w = np.ascontiguousarray(inp["topk_w"][:n])
+    srb = xs_rows.shape[1] if fp8 else 0
+    times = []
+    t_start = time.perf_counter()
+    for _ in range(max_reps):
+        t0 = time.perf_counter()
+        lay = oracle.layout(idx, E, R)
+        d = oracle.layout_dedup(idx, E, R)
+        dregs, dsregs, _ = oracle.dispatch_dedup(x_rows, xs_rows, idx, d["tok_pos"],
+                                                 d["tok_offset"], E, R, d["tok_count"])
+        regs, _, _ = oracle.expand(dregs, dsregs, srb, idx, lay["pos"], lay["rank_offset"],
+                                   d["tok_pos"], d["tok_offset"], d["tok_count"], E, R,
+                                   lay["rank_count"])
+        t1 = time.perf_counter()
+        if fp8:
+            ey = [np.zeros((r.shape[0], H), np.uint16) for r in regs]
+        else:
+            ey = [r.view(np.uint16).reshape(r.shape[0], H) for r in regs]
+        t2 = time.perf_counter()
+        parts, _ = oracle.combine_local(ey, w, idx, lay["pos"], lay["rank_offset"],
+                                        lay["rank_count"], d["tok_pos"], d["tok_offset"],
+                                        d["tok_count"], E, R, H)
+        oracle.combine_dedup(parts, idx, d["tok_pos"], d["tok_offset"], d["tok_count"], E, R,
+                             H)
+        t3 = time.perf_counter()
+        times.append((t1 - t0) + (t3 - t2))
+        del dregs, regs, ey, parts
         if time.perf_counter() - t_start > budget_s:
             break
     return float(np.median(times)), len(times)
@@ -358,7 +409,20 @@ def dedup_bench(a):
         "dedup_step_us": round(dedup_step, 2),
         "per_slot_step_us": round(slot_step, 2),
         "status": st,
+        "cpu_baseline": None,
     }
+    if not a.no_cpu_baseline:
+        print("[dedup] timing the CPU oracle", file=sys.stderr, flush=True)
+        n_s = min(T, 2048)   # a bounded sample: the first n_s tokens
+        cpu_s, reps = cpu_baseline_dedup(cfg, inp, n_s)
+        full_us = cpu_s * 1e6 * T / n_s
+        out["cpu_baseline"] = {
+            "step_us": round(full_us, 1), "unit": "us per full step (scaled)", "cores": 1,
+            "kind": "oracle",
+            "sample": f"first {n_s} of {T} tokens (both layouts, pair dispatch, expansion, "
+                      f"partial combine, source sum), median of {reps} run(s), {cpu_s:.2f} s "
+                      f"each, scaled by {T}/{n_s}; 1 thread, host CPU: {cpu_model()}",
+            "gpu_speedup": round(full_us / dedup_step, 1), "host_nproc": os.cpu_count()}
     print(json.dumps(out), flush=True)
     return 0 if st == 0 else 1
 
@@ -618,11 +682,12 @@ def main(argv=None):
 
     if not a.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        cpu_s, reps = cpu_baseline(cfg, inp)
+        cpu_s, reps = cpu_baseline(cfg, inp, capacity=capacity)
         out["cpu_baseline"] = {
             "value": round(dc_bytes / cpu_s / 1e9, 3), "unit": "GB/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"full workload (layout+dispatch+combine), median of {reps} run(s), "
+            "sample": f"full workload ({'fixed-capacity ' if capacity else ''}layout+"
+                      f"dispatch+combine), median of {reps} run(s), "
                       f"{cpu_s:.2f} s each, 1 thread, host CPU: {cpu_model()}",
             "tokens_per_s": round(T / cpu_s, 1), "host_nproc": os.cpu_count()}
     print(json.dumps(out), flush=True)
