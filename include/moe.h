@@ -79,10 +79,11 @@ extern "C" {
 #define MOE_FP8_BLOCK 128
 
 /* Number of parts of the byte-balanced partition plan.  moe_dispatch and
- * moe_combine launch W wavefronts, W the number the GPU keeps resident for
- * the kernel (rounded down to a divisor of MOE_PLAN_PARTS), and wavefront g
- * takes the contiguous parts [g*P/W, (g+1)*P/W).  12288 = 3 * 2^12 divides
- * evenly over 256 compute units at 4, 8, 12, 16, 24 or 48 wavefronts each. */
+ * moe_combine launch W wavefronts, W a power of two (512 to 4096, sized
+ * from the bytes each wavefront keeps in flight) that divides P, and
+ * wavefront g takes parts g, g+W, g+2W, ... (P/W parts of equal byte cost).
+ * 12288 = 3 * 2^12 also divides evenly over 256 compute units at 4, 8, 12,
+ * 16, 24 or 48 wavefronts each. */
 #define MOE_PLAN_PARTS 12288
 
 /* Library version (MOE_VERSION). */
@@ -215,8 +216,10 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
  *              the workspace (moe_layout zeroes it; the last wavefront resets
  *              it), so faster wavefronts take more parts.  Calls that share a
  *              workspace must not run concurrently under this policy.
- * waves        wavefronts to launch: 0 launches as many as the device holds
- *              at once (the product choice); otherwise a multiple of 4 that
+ * waves        wavefronts to launch: 0 lets the library choose (the product
+ *              choice; the push policies use the count of moe_dispatch, the
+ *              pull policies as many as the device holds at once); otherwise
+ *              a multiple of 4 that
  *              divides MOE_PLAN_PARTS (and, under MOE_POLICY_BY_RANK, a
  *              multiple of R), else MOE_EINVAL.  Fewer wavefronts occupy fewer
  *              compute units: sweeping the count shows how each split's

@@ -35,6 +35,17 @@ int resident_waves(const void* kernel, size_t lds_bytes) {
   return w;
 }
 
+int copy_waves(const void* kernel, int64_t per_wave, int64_t target) {
+  const int cap = resident_waves(kernel, 0);
+  int hi = kWavesPerBlock;
+  while (hi * 2 <= cap) hi *= 2;
+  const int lo = hi < 512 ? hi : 512;
+  const double want = (double)target / (double)(per_wave > 0 ? per_wave : 1);
+  int w = lo;
+  while (w < hi && (double)w * 1.41421356 < want) w *= 2;
+  return w;
+}
+
 }  // namespace moe
 
 namespace {
@@ -148,7 +159,7 @@ int dispatch_common(const void* x, const float* x_scales, int dtype, int64_t T, 
                     const uint64_t* recv_scales, int scale_pitch, const int32_t* recv_cap,
                     const void* workspace, size_t workspace_bytes, size_t need_bytes,
                     size_t ticket_offset, uint32_t* status, int policy, int waves,
-                    uint64_t* trace, int trace_waves, void* stream) {
+                    uint64_t* trace, int trace_waves, int rows_hint, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1 || (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3)) return MOE_EINVAL;
@@ -196,6 +207,7 @@ int dispatch_common(const void* x, const float* x_scales, int dtype, int64_t T, 
   a.trace = trace;
   a.trace_waves = trace ? trace_waves : 0;
   a.launch_waves = waves;
+  a.rows_hint = rows_hint;
   return launched(moe::launch_dispatch(a, policy, as_stream(stream)));
 }
 
@@ -215,7 +227,7 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
   return dispatch_common(x, x_scales, dtype, T, H, k, E, R, topk_idx, pos, rank_offset, row_src,
                          recv_x, recv_scales, scale_pitch, recv_cap, workspace, workspace_bytes,
                          g.total, g.ticket_offset, status, policy, waves, trace, trace_waves,
-                         stream);
+                         0, stream);
 }
 
 int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k, int E,
@@ -238,7 +250,7 @@ int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weig
                    const int32_t* rank_offset, const int32_t* recv_cap, uint16_t* y,
                    const void* workspace, size_t workspace_bytes, size_t need_bytes,
                    size_t ticket_offset, uint32_t* status, int policy, int waves,
-                   uint64_t* trace, int trace_waves, void* stream) {
+                   uint64_t* trace, int trace_waves, int rows_hint, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
   if (H < 1) return MOE_EINVAL;
@@ -266,6 +278,7 @@ int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weig
   a.trace = trace;
   a.trace_waves = trace ? trace_waves : 0;
   a.launch_waves = waves;
+  a.rows_hint = rows_hint;
   a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
                                           ticket_offset) + 2;
   return launched(moe::launch_combine(a, policy, as_stream(stream)));
@@ -285,7 +298,7 @@ int moe_combine_ex(const uint64_t* expert_y, const float* topk_w, int64_t T, int
   const moe::LayoutGeom g = moe::layout_geom(T, E);
   return combine_common(expert_y, topk_w, false, T, H, k, E, R, topk_idx, pos, rank_offset,
                         recv_cap, y, workspace, workspace_bytes, g.total, g.ticket_offset,
-                        status, policy, waves, trace, trace_waves, stream);
+                        status, policy, waves, trace, trace_waves, 0, stream);
 }
 
 int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k, int E,
@@ -371,7 +384,7 @@ int moe_dispatch_dedup(const void* x, const float* x_scales, int dtype, int64_t 
   return dispatch_common(x, x_scales, dtype, T, H, k, E, R, topk_idx, tok_pos, tok_offset,
                          nullptr, recv_x, recv_scales, scale_pitch, recv_cap, workspace,
                          workspace_bytes, d.total, d.g.ticket_offset, status,
-                         MOE_POLICY_BALANCED, 0, nullptr, 0, stream);
+                         MOE_POLICY_BALANCED, 0, nullptr, 0, (k + 1) / 2, stream);
 }
 
 int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype, int64_t T,
@@ -416,7 +429,6 @@ int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype,
   a.tok_pos = tok_pos;
   a.tok_offset = tok_offset;
   a.bound = static_cast<const int32_t*>(workspace);
-  a.parts_per_wave = 0;
   a.status = status;
   return launched(moe::launch_expand(a, as_stream(stream)));
 }
@@ -453,7 +465,6 @@ int moe_combine_local(const uint64_t* expert_y, const float* topk_w, int64_t T, 
   a.tok_pos = tok_pos;
   a.tok_offset = tok_offset;
   a.bound = static_cast<const int32_t*>(workspace);
-  a.parts_per_wave = 0;
   a.status = status;
   return launched(moe::launch_combine_local(a, as_stream(stream)));
 }
@@ -467,7 +478,8 @@ int moe_combine_dedup(const uint64_t* partial, int64_t T, int H, int k, int E, i
   const moe::DedupGeom d = moe::dedup_geom(T, k, R);
   return combine_common(partial, nullptr, true, T, H, k, E, R, topk_idx, tok_pos, tok_offset,
                         part_cap, y, workspace, workspace_bytes, d.total, d.g.ticket_offset,
-                        status, MOE_POLICY_BALANCED, 0, nullptr, 0, stream);
+                        status, MOE_POLICY_BALANCED, 0, nullptr, 0,
+                        (moe::slot_width(k) + 1) / 2, stream);
 }
 
 }  // extern "C"

@@ -1,7 +1,7 @@
 // Combine: y[t] = bf16( sum_j w[t,j] * Y(row of slot j) ).
 //
 // Token-centric gather-reduce with the same byte-balanced partition as
-// dispatch (one wavefront per part of the plan).  Slot metadata for a batch
+// dispatch (wavefront g of W takes parts g, g + W, ... of the plan).  Slot metadata for a batch
 // of 64/k tokens is resolved once, one slot per lane, and parked in LDS; for
 // each token the wavefront reads its k source rows and weights back at
 // uniform LDS addresses (waiting only on the LDS counter, never on pending
@@ -110,7 +110,6 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
   const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
   const uint64_t t_start = a.trace ? (uint64_t)wall_clock64() : 0;
   const int W = gridDim.x * kWavesPerBlock;
-  const int m = DYN ? 1 : a.parts_per_wave;  // plan parts per unit of work
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t l16 = lane * kVecBytes;
   const int k = a.k;
@@ -123,9 +122,9 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
     s_w[wv][kWave + lane] = 0.0f;
   }
 
-  for (int chunk = g; chunk * m < MOE_PLAN_PARTS;
-       chunk = DYN ? next_chunk<DYN>(a.tickets, W, lane) : MOE_PLAN_PARTS) {
-  const int t0 = a.bound[chunk * m], t1 = a.bound[(chunk + 1) * m];
+  for (int part = g; part < MOE_PLAN_PARTS;
+       part = DYN ? next_chunk<DYN>(a.tickets, W, lane) : part + W) {
+  const int t0 = a.bound[part], t1 = a.bound[part + 1];
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t srow = 0;
@@ -192,8 +191,12 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
 template <int KW, bool DYN>
 hipError_t launch_kw(CombineArgs a, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&combine_kernel<KW, DYN>);
-  const int waves = a.launch_waves > 0 ? a.launch_waves : resident_waves(fn, 0);
-  a.parts_per_wave = MOE_PLAN_PARTS / waves;
+  // KW gathers of 1 KiB for each of the two segments in flight (of which
+  // rows_hint read routed rows when the caller expects masked slots)
+  const int64_t rows = a.rows_hint > 0 ? a.rows_hint : KW;
+  const int waves = a.launch_waves > 0
+                        ? a.launch_waves
+                        : copy_waves(fn, 2 * rows * kWaveBytes, kCombineInFlight);
   hipLaunchKernelGGL((combine_kernel<KW, DYN>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
                      stream, a);
   return hipGetLastError();

@@ -44,7 +44,6 @@ struct ExpandArgs {
   const int32_t* tok_pos;
   const int32_t* tok_offset;
   const int32_t* bound;          // plan of the per-slot layout
-  int32_t parts_per_wave;
   uint32_t* status;
 };
 
@@ -65,7 +64,6 @@ struct LocalArgs {
   const int32_t* tok_pos;
   const int32_t* tok_offset;
   const int32_t* bound;          // plan of the per-slot layout
-  int32_t parts_per_wave;
   uint32_t* status;
 };
 

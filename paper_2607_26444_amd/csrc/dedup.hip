@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
   const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
-  const int m = a.parts_per_wave;
+  const int W = gridDim.x * kWavesPerBlock;
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t sb = (uint32_t)a.scale_row_bytes;
   const uint32_t sp = (uint32_t)a.scale_pitch;
@@ -112,7 +112,8 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
   const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
   uint32_t st = 0;
 
-  const int t0 = a.bound[g * m], t1 = a.bound[(g + 1) * m];
+  for (int part = g; part < MOE_PLAN_PARTS; part += W) {
+  const int t0 = a.bound[part], t1 = a.bound[part + 1];
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -210,6 +211,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
       }
     }
   }
+  }
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
 }
@@ -279,7 +281,7 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
   const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
-  const int m = a.parts_per_wave;
+  const int W = gridDim.x * kWavesPerBlock;
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t l16 = lane * kVecBytes;
   const int k = a.k;
@@ -294,7 +296,8 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
     s_last[wv][kWave + lane] = 0;
   }
 
-  const int t0 = a.bound[g * m], t1 = a.bound[(g + 1) * m];
+  for (int part = g; part < MOE_PLAN_PARTS; part += W) {
+  const int t0 = a.bound[part], t1 = a.bound[part + 1];
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -409,6 +412,7 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
       }
     }
   }
+  }
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
 }
@@ -418,8 +422,9 @@ hipError_t launch_expand_vpl(ExpandArgs a, hipStream_t stream) {
   const bool full = a.row_bytes == (int64_t)VPL * kWaveBytes;
   const void* fn = full ? reinterpret_cast<const void*>(&expand_kernel<VPL, true, SCALES>)
                         : reinterpret_cast<const void*>(&expand_kernel<VPL, false, SCALES>);
-  const int waves = resident_waves(fn, 0);
-  a.parts_per_wave = MOE_PLAN_PARTS / waves;
+  // a token's pair rows are loaded one after another: about half of
+  // dispatch's stores are in flight per wavefront
+  const int waves = copy_waves(fn, (int64_t)(a.k + 1) / 2 * a.row_bytes, kDispatchInFlight);
   const dim3 grid(waves / kWavesPerBlock), block(kBlock);
   if (full)
     hipLaunchKernelGGL((expand_kernel<VPL, true, SCALES>), grid, block, 0, stream, a);
@@ -454,8 +459,8 @@ hipError_t launch_expand_scales(const ExpandArgs& a, hipStream_t stream) {
 template <int KW>
 hipError_t launch_local_kw(LocalArgs a, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&combine_local_kernel<KW>);
-  const int waves = resident_waves(fn, 0);
-  a.parts_per_wave = MOE_PLAN_PARTS / waves;
+  const int waves =
+      copy_waves(fn, (KW >= 32 ? 1ll : 2ll) * KW * kWaveBytes, kCombineInFlight);
   hipLaunchKernelGGL((combine_local_kernel<KW>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
                      stream, a);
   return hipGetLastError();

@@ -3,10 +3,14 @@
 // Work split (Section 6.2 with one memory tier, Appendix D third level):
 // moe_layout leaves MOE_PLAN_PARTS contiguous token ranges of equal byte
 // cost (a token costs one row read plus one row write per routed slot).  The
-// kernel launches as many wavefronts as the GPU keeps resident and gives
-// each the same number of consecutive parts, so every wavefront moves the
-// same number of bytes no matter how skewed the routing is; a hot expert only
-// changes where rows land, not who copies them.
+// kernel launches W wavefronts (a power of two chosen by copy_waves) and
+// wavefront g takes parts g, g + W, g + 2W, ...: every wavefront moves the
+// same number of bytes no matter how skewed the routing is (a hot expert only
+// changes where rows land, not who copies them), and at any moment the W
+// wavefronts work on neighbouring parts, so x is read and each expert window
+// is written as one advancing front instead of W scattered streams (on
+// MI355X that measured ~5% faster for dispatch and ~7% for combine than
+// giving each wavefront one contiguous run of parts).
 //
 // Push direction: a wavefront reads its token's row from x once into
 // registers (16 bytes per lane per 1 KiB segment, so a 14 KiB row is 14
@@ -38,7 +42,6 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
   const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
   const uint64_t t_start = a.trace ? (uint64_t)wall_clock64() : 0;
   const int W = gridDim.x * kWavesPerBlock;
-  const int m = DYN ? 1 : a.parts_per_wave;  // plan parts per unit of work
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t sb = (uint32_t)a.scale_row_bytes;
   const uint32_t sp = (uint32_t)a.scale_pitch;
@@ -53,9 +56,9 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     if (SCALES) s_sdst[wv][kWave + lane] = 0;
   }
 
-  for (int chunk = g; chunk * m < MOE_PLAN_PARTS;
-       chunk = DYN ? next_chunk<DYN>(a.tickets, W, lane) : MOE_PLAN_PARTS) {
-  const int t0 = a.bound[chunk * m], t1 = a.bound[(chunk + 1) * m];
+  for (int part = g; part < MOE_PLAN_PARTS;
+       part = DYN ? next_chunk<DYN>(a.tickets, W, lane) : part + W) {
+  const int t0 = a.bound[part], t1 = a.bound[part + 1];
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t dst = 0, sdst = 0;
@@ -267,8 +270,10 @@ hipError_t launch_push(DispatchArgs a, hipStream_t stream) {
   const void* fn =
       full ? reinterpret_cast<const void*>(&dispatch_kernel<VPL, true, SCALES, DYN>)
            : reinterpret_cast<const void*>(&dispatch_kernel<VPL, false, SCALES, DYN>);
-  const int waves = a.launch_waves > 0 ? a.launch_waves : resident_waves(fn, 0);
-  a.parts_per_wave = MOE_PLAN_PARTS / waves;
+  const int64_t rows = a.rows_hint > 0 ? a.rows_hint : a.k;
+  const int waves = a.launch_waves > 0
+                        ? a.launch_waves
+                        : copy_waves(fn, rows * a.row_bytes, kDispatchInFlight);
   const dim3 grid(waves / kWavesPerBlock), block(kBlock);
   if (full)
     hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES, DYN>), grid, block, 0, stream, a);

@@ -45,6 +45,17 @@ int slot_width(int k);
 // of kWavesPerBlock.  Queried once per (device, kernel) and cached.
 int resident_waves(const void* kernel, size_t lds_bytes);
 
+// Wavefronts for a byte-balanced copy kernel with `per_wave` bytes of memory
+// operations in flight per wavefront: the power of two nearest to
+// target / per_wave, between 512 and the resident count.  Each wavefront
+// takes every W-th part of the plan, so the W wavefronts sweep the tokens as
+// one front; on MI355X a front with about 64 MiB of dispatch stores (16 MiB
+// of combine gathers) in flight, and whole workgroups per compute unit,
+// measured fastest.
+int copy_waves(const void* kernel, int64_t per_wave, int64_t target);
+constexpr int64_t kDispatchInFlight = 64ll << 20;
+constexpr int64_t kCombineInFlight = 16ll << 20;
+
 // fixed_cap < 0: packed layout; >= 0: fixed windows of fixed_cap rows.
 hipError_t launch_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
                          int fixed_cap, int32_t* expert_count, int32_t* expert_offset,
@@ -67,8 +78,8 @@ struct DispatchArgs {
   const uint64_t* recv_scales;
   const int32_t* recv_cap;
   const int32_t* bound;        // plan: bound[MOE_PLAN_PARTS + 1]
-  int32_t parts_per_wave;      // MOE_PLAN_PARTS / launched wavefronts
-  int32_t launch_waves;        // wavefronts to launch; 0 = as many as are resident
+  int32_t launch_waves;        // wavefronts to launch; 0 = copy_waves' choice
+  int32_t rows_hint;           // rows written per token, for copy_waves (0: k)
   uint32_t* status;
   const int32_t* row_src;      // pull policies only
   int32_t R;
@@ -91,8 +102,8 @@ struct CombineArgs {
   const int32_t* recv_cap;
   uint16_t* y;
   const int32_t* bound;
-  int32_t parts_per_wave;
   int32_t launch_waves;
+  int32_t rows_hint;           // rows gathered per token, for copy_waves (0: all KW)
   uint32_t* status;
   uint64_t* trace;
   int32_t trace_waves;

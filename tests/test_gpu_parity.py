@@ -243,13 +243,16 @@ def test_fixed_capacity_step_in_a_captured_graph():
 
 
 def test_trace_records_every_wavefront():
+    from paper_2607_26444_amd import moe
     h = _h()
     cfg = wl.custom(3000, 7168, 256, 64, 8, zipf_s=1.2, seed=5)
     run = h.GpuRun(cfg, wl.make_inputs(cfg), trace=True)
     for tr in (run.dtrace, run.ctrace):
         t = tr.view(-1, 2).cpu().numpy()
         used = t[:, 0] != 0
-        assert used.sum() >= 1024          # one record per launched wavefront
+        n = int(used.sum())                # one record per launched wavefront:
+        assert np.all(used[:n])            # wavefronts 0 .. W-1, W a power of two
+        assert n >= 512 and n & (n - 1) == 0 and moe.MOE_PLAN_PARTS % n == 0
         assert np.all(t[used, 1] >= t[used, 0])
         assert np.all(t[~used] == 0)
         span = t[used, 1].max() - t[used, 0].min()
