@@ -122,9 +122,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
     s_w[wv][kWave + lane] = 0.0f;
   }
 
-  for (int part = g; part < MOE_PLAN_PARTS;
-       part = DYN ? next_chunk<DYN>(a.tickets, W, lane) : part + W) {
-  const int t0 = a.bound[part], t1 = a.bound[part + 1];
+  for_each_part<DYN>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t srow = 0;
@@ -181,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
       }
     }
   }
-  }
+  });
   finish_chunks<DYN>(a.tickets, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);

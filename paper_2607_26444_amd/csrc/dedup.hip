@@ -112,8 +112,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
   const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
   uint32_t st = 0;
 
-  for (int part = g; part < MOE_PLAN_PARTS; part += W) {
-  const int t0 = a.bound[part], t1 = a.bound[part + 1];
+  for_each_part<false>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -211,7 +210,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
       }
     }
   }
-  }
+  });
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
 }
@@ -296,8 +295,7 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
     s_last[wv][kWave + lane] = 0;
   }
 
-  for (int part = g; part < MOE_PLAN_PARTS; part += W) {
-  const int t0 = a.bound[part], t1 = a.bound[part + 1];
+  for_each_part<false>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -412,7 +410,7 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
       }
     }
   }
-  }
+  });
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
 }

@@ -56,9 +56,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     if (SCALES) s_sdst[wv][kWave + lane] = 0;
   }
 
-  for (int part = g; part < MOE_PLAN_PARTS;
-       part = DYN ? next_chunk<DYN>(a.tickets, W, lane) : part + W) {
-  const int t0 = a.bound[part], t1 = a.bound[part + 1];
+  for_each_part<DYN>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t dst = 0, sdst = 0;
@@ -126,7 +124,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
       }
     }
   }
-  }
+  });
   finish_chunks<DYN>(a.tickets, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);

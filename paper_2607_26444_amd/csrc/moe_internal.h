@@ -189,6 +189,33 @@ __device__ __forceinline__ void finish_chunks(uint32_t* tickets, int W, int lane
   }
 }
 
+// Visits the token range [t0, t1) of every plan part wavefront g owns.
+// Static: parts g, g + W, g + 2W, ...; their boundaries are fetched 64 at a
+// time, one part per lane, so stepping to the next part (often an empty one
+// when there are fewer tokens than parts) costs no global-memory round trip.
+// Dynamic: part g, then parts claimed from the ticket counter.
+template <bool DYN, typename F>
+__device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* tickets, int g,
+                                              int W, int lane, F&& body) {
+  if (DYN) {
+    for (int part = g; part < MOE_PLAN_PARTS; part = next_chunk<DYN>(tickets, W, lane))
+      body((int)ld4(bound + part), (int)ld4(bound + part + 1));
+    return;
+  }
+  const int m = (MOE_PLAN_PARTS - g + W - 1) / W;   // parts g + i*W < MOE_PLAN_PARTS
+  for (int i0 = 0; i0 < m; i0 += kWave) {
+    int b0 = 0, b1 = 0;
+    if (i0 + lane < m) {
+      const int part = g + (i0 + lane) * W;
+      b0 = (int)ld4(bound + part);
+      b1 = (int)ld4(bound + part + 1);
+    }
+    const int n = m - i0 < kWave ? m - i0 : kWave;
+    for (int i = 0; i < n; ++i)
+      body(__builtin_amdgcn_readlane(b0, i), __builtin_amdgcn_readlane(b1, i));
+  }
+}
+
 // Per-wavefront trace record (start, end) in the constant-rate wall clock.
 // The end stamp is taken after the wavefront's stores have completed.
 __device__ __forceinline__ void trace_wave(uint64_t* trace, int trace_waves, int g,
