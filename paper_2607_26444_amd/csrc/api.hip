@@ -35,11 +35,11 @@ int resident_waves(const void* kernel, size_t lds_bytes) {
   return w;
 }
 
-int copy_waves(const void* kernel, int64_t per_wave, int64_t target) {
+int copy_waves(const void* kernel, int64_t per_wave, int64_t target, int min_waves) {
   const int cap = resident_waves(kernel, 0);
   int hi = kWavesPerBlock;
   while (hi * 2 <= cap) hi *= 2;
-  const int lo = hi < 512 ? hi : 512;
+  const int lo = hi < min_waves ? hi : min_waves;
   const double want = (double)target / (double)(per_wave > 0 ? per_wave : 1);
   int w = lo;
   while (w < hi && (double)w * 1.41421356 < want) w *= 2;

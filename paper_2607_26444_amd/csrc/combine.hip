@@ -194,7 +194,7 @@ hipError_t launch_kw(CombineArgs a, hipStream_t stream) {
   const int64_t rows = a.rows_hint > 0 ? a.rows_hint : KW;
   const int waves = a.launch_waves > 0
                         ? a.launch_waves
-                        : copy_waves(fn, 2 * rows * kWaveBytes, kCombineInFlight);
+                        : copy_waves(fn, 2 * rows * kWaveBytes, kCombineInFlight, 512);
   hipLaunchKernelGGL((combine_kernel<KW, DYN>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
                      stream, a);
   return hipGetLastError();

@@ -186,11 +186,11 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
 #pragma unroll
           for (int c = 0; c < VPL; ++c) {
             const uint32_t off = seg + c * kWaveBytes + l16;
-            if (FULL || off < rb) st16(dj + off, v[c]);
+            if (FULL || off < rb) st16_stream(dj + off, v[c]);
           }
           if (s16 && seg == 0) {
             uint8_t* sd = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l0 + j], 0));
-            if (l16 < sp) st16(sd + l16, sv);
+            if (l16 < sp) st16_stream(sd + l16, sv);
           }
         }
       }
@@ -422,7 +422,8 @@ hipError_t launch_expand_vpl(ExpandArgs a, hipStream_t stream) {
                         : reinterpret_cast<const void*>(&expand_kernel<VPL, false, SCALES>);
   // a token's pair rows are loaded one after another: about half of
   // dispatch's stores are in flight per wavefront
-  const int waves = copy_waves(fn, (int64_t)(a.k + 1) / 2 * a.row_bytes, kDispatchInFlight);
+  const int waves =
+      copy_waves(fn, (int64_t)(a.k + 1) / 2 * a.row_bytes, kDispatchInFlight, 256);
   const dim3 grid(waves / kWavesPerBlock), block(kBlock);
   if (full)
     hipLaunchKernelGGL((expand_kernel<VPL, true, SCALES>), grid, block, 0, stream, a);
@@ -458,7 +459,7 @@ template <int KW>
 hipError_t launch_local_kw(LocalArgs a, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&combine_local_kernel<KW>);
   const int waves =
-      copy_waves(fn, (KW >= 32 ? 1ll : 2ll) * KW * kWaveBytes, kCombineInFlight);
+      copy_waves(fn, (KW >= 32 ? 1ll : 2ll) * KW * kWaveBytes, kCombineInFlight, 512);
   hipLaunchKernelGGL((combine_local_kernel<KW>), dim3(waves / kWavesPerBlock), dim3(kBlock), 0,
                      stream, a);
   return hipGetLastError();

@@ -16,7 +16,9 @@
 // registers (16 bytes per lane per 1 KiB segment, so a 14 KiB row is 14
 // dwordx4 loads in flight per lane) and stores it to each of the token's k
 // destinations.  x is read exactly once; every destination row is written
-// by exactly one wavefront with full 1 KiB coalesced stores.  Slot metadata
+// by exactly one wavefront with full 1 KiB coalesced stores, non-temporal
+// (written once, not read again here; with the advancing front this measured
+// 8-12% faster than ordinary stores on MI355X).  Slot metadata
 // (pos, expert, region base, capacity) for a batch of 64/k tokens is loaded
 // once, one slot per lane, and parked in LDS; the copy loop reads each
 // destination back at a uniform LDS address, so no global load of metadata
@@ -102,11 +104,11 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
 #pragma unroll
           for (int c = 0; c < VPL; ++c) {
             const uint32_t off = seg + c * kWaveBytes + l16;
-            if (FULL || off < rb) st16(d + off, v[c]);
+            if (FULL || off < rb) st16_stream(d + off, v[c]);
           }
           if (s16 && seg == 0) {
             uint8_t* sd = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l0 + j], 0));
-            if (l16 < sp) st16(sd + l16, sv);
+            if (l16 < sp) st16_stream(sd + l16, sv);
           }
         }
       }
@@ -271,7 +273,7 @@ hipError_t launch_push(DispatchArgs a, hipStream_t stream) {
   const int64_t rows = a.rows_hint > 0 ? a.rows_hint : a.k;
   const int waves = a.launch_waves > 0
                         ? a.launch_waves
-                        : copy_waves(fn, rows * a.row_bytes, kDispatchInFlight);
+                        : copy_waves(fn, rows * a.row_bytes, kDispatchInFlight, 256);
   const dim3 grid(waves / kWavesPerBlock), block(kBlock);
   if (full)
     hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES, DYN>), grid, block, 0, stream, a);

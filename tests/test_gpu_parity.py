@@ -252,7 +252,7 @@ def test_trace_records_every_wavefront():
         used = t[:, 0] != 0
         n = int(used.sum())                # one record per launched wavefront:
         assert np.all(used[:n])            # wavefronts 0 .. W-1, W a power of two
-        assert n >= 512 and n & (n - 1) == 0 and moe.MOE_PLAN_PARTS % n == 0
+        assert n >= 256 and n & (n - 1) == 0 and moe.MOE_PLAN_PARTS % n == 0
         assert np.all(t[used, 1] >= t[used, 0])
         assert np.all(t[~used] == 0)
         span = t[used, 1].max() - t[used, 0].min()
