@@ -244,6 +244,7 @@ def ablation(a):
         return rec
 
     for name, pol in (("balanced_push", moe.MOE_POLICY_BALANCED),
+                      ("static_push", moe.MOE_POLICY_STATIC),
                       ("dynamic_push", moe.MOE_POLICY_DYNAMIC),
                       ("rows_pull", moe.MOE_POLICY_ROWS),
                       ("by_rank_pull", moe.MOE_POLICY_BY_RANK)):
@@ -258,6 +259,7 @@ def ablation(a):
             continue
         rec = {"waves": waves}
         for name, pol in (("balanced_push", moe.MOE_POLICY_BALANCED),
+                          ("static_push", moe.MOE_POLICY_STATIC),
                           ("by_rank_pull", moe.MOE_POLICY_BY_RANK)):
             r = time_dispatch(pol, waves)
             rec[name] = {k2: r[k2] for k2 in ("dispatch_us", "GBps", "completion_gap_pct")}
@@ -269,7 +271,7 @@ def ablation(a):
         y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
         out["combine"] = {}
         for name, pol in (("balanced", moe.MOE_POLICY_BALANCED),
-                          ("dynamic", moe.MOE_POLICY_DYNAMIC)):
+                          ("dynamic", moe.MOE_POLICY_DYNAMIC)):   # balanced = static here
             def runc(tr=None):
                 moe.moe_combine_ex(regions.table, w_d, H, E, R, idx_d, lay.pos,
                                    lay.rank_offset, regions.cap, y, lay.workspace, lay.status,

@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define MOE_VERSION 3
+#define MOE_VERSION 4
 
 #define MOE_OK 0
 #define MOE_EINVAL (-1)
@@ -187,7 +187,11 @@ int moe_layout_fixed(const int32_t* topk_idx, int64_t T, int k, int E, int R, in
  *           wavefronts write partially; packed 224-byte rows cost ~30 us more
  *           per 131k rows on MI355X.
  * recv_cap  [R] int32 capacity of each region in rows.
- * topk_idx, pos, rank_offset, workspace: as produced by moe_layout.
+ * topk_idx, pos, rank_offset, workspace: as produced by moe_layout.  The
+ *           second half of the plan's parts is handed out at run time from
+ *           a counter in the workspace (MOE_POLICY_BALANCED of
+ *           moe_dispatch_ex): two dispatch calls that share a workspace must
+ *           not run at the same time on different streams.
  * Bytes of a region beyond the rows dispatch writes are left untouched.
  */
 int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int H,
@@ -197,11 +201,17 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
                  const void* workspace, size_t workspace_bytes, uint32_t* status,
                  void* stream);
 
-/* Work-split policies of moe_dispatch_ex (all give bit-identical regions). */
-#define MOE_POLICY_BALANCED 0 /* byte-balanced token ranges, push (moe_dispatch) */
+/* Work-split policies of moe_dispatch_ex / moe_combine_ex (all give
+ * bit-identical regions and identical y). */
+#define MOE_POLICY_BALANCED 0 /* byte-balanced parts, the library's choice: dispatch
+                               * assigns the first half of the parts statically and
+                               * hands the rest out at run time (all statically when
+                               * a wavefront would own fewer than 8 parts); combine
+                               * assigns all statically (moe_dispatch, moe_combine) */
 #define MOE_POLICY_ROWS 1     /* pull: the N routed rows split evenly over wavefronts */
 #define MOE_POLICY_BY_RANK 2  /* pull: a fixed group of W/R wavefronts per rank */
-#define MOE_POLICY_DYNAMIC 3  /* push; byte-balanced parts handed out at run time */
+#define MOE_POLICY_DYNAMIC 3  /* push; every part after the first handed out at run time */
+#define MOE_POLICY_STATIC 4   /* push; every part assigned statically (parts g, g+W, ...) */
 
 /*
  * moe_dispatch_ex -- moe_dispatch with a choice of work split and an
@@ -210,12 +220,15 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
  * one; MOE_POLICY_BY_RANK is that naive assignment, MOE_POLICY_ROWS splits
  * the same pull work evenly, MOE_POLICY_BALANCED is the product path).
  *
- * policy       one of MOE_POLICY_*; anything else is MOE_EINVAL.  With
- *              MOE_POLICY_DYNAMIC each wavefront starts with one part of the
- *              plan and then claims the next unclaimed part from a counter in
- *              the workspace (moe_layout zeroes it; the last wavefront resets
- *              it), so faster wavefronts take more parts.  Calls that share a
- *              workspace must not run concurrently under this policy.
+ * policy       one of MOE_POLICY_*; anything else is MOE_EINVAL.  Parts
+ *              handed out at run time (MOE_POLICY_DYNAMIC, and the second half
+ *              under MOE_POLICY_BALANCED) are claimed in plan order from a
+ *              counter in the workspace (moe_layout zeroes it; the last
+ *              wavefront of a launch resets it), so faster wavefronts take
+ *              more parts.  Dispatch calls that share a workspace must
+ *              therefore not run concurrently under these policies (nor
+ *              combine calls under MOE_POLICY_DYNAMIC); calls one after
+ *              another on a stream, or replayed in a graph, are fine.
  * waves        wavefronts to launch: 0 lets the library choose (the product
  *              choice; the push policies use the count of moe_dispatch, the
  *              pull policies as many as the device holds at once); otherwise
@@ -261,8 +274,9 @@ int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H,
                 void* stream);
 
 /*
- * moe_combine_ex -- moe_combine with a work split (MOE_POLICY_BALANCED or
- * MOE_POLICY_DYNAMIC, as for moe_dispatch_ex; others are MOE_EINVAL), the
+ * moe_combine_ex -- moe_combine with a work split (MOE_POLICY_BALANCED and
+ * MOE_POLICY_STATIC: all parts assigned statically; MOE_POLICY_DYNAMIC as
+ * for moe_dispatch_ex; others are MOE_EINVAL), the
  * wavefront count and the optional per-wavefront trace of moe_dispatch_ex
  * (same rules, layout and clock).
  */

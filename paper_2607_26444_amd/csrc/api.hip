@@ -168,7 +168,8 @@ int dispatch_common(const void* x, const float* x_scales, int dtype, int64_t T, 
   if (fp8 && (!x_scales || !recv_scales)) return MOE_EINVAL;
   if (T > 0 && (!x || !topk_idx || !pos)) return MOE_EINVAL;
   if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_ROWS &&
-      policy != MOE_POLICY_BY_RANK && policy != MOE_POLICY_DYNAMIC)
+      policy != MOE_POLICY_BY_RANK && policy != MOE_POLICY_DYNAMIC &&
+      policy != MOE_POLICY_STATIC)
     return MOE_EINVAL;
   const bool pull = policy == MOE_POLICY_ROWS || policy == MOE_POLICY_BY_RANK;
   if (pull && T > 0 && !row_src) return MOE_EINVAL;
@@ -256,7 +257,9 @@ int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weig
   if (H < 1) return MOE_EINVAL;
   if (!expert_y || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
   if (T > 0 && ((!unit_weights && !topk_w) || !topk_idx || !pos || !y)) return MOE_EINVAL;
-  if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_DYNAMIC) return MOE_EINVAL;
+  if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_DYNAMIC &&
+      policy != MOE_POLICY_STATIC)
+    return MOE_EINVAL;
   if (!waves_ok(waves)) return MOE_EINVAL;
   if (trace && trace_waves < 0) return MOE_EINVAL;
   if ((2 * (int64_t)H) % 16 != 0 || !aligned(y, 16)) return MOE_EALIGN;

@@ -122,7 +122,8 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
     s_w[wv][kWave + lane] = 0.0f;
   }
 
-  for_each_part<DYN>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
+  for_each_part<DYN ? kPartsClaimed : kPartsStatic>(a.bound, a.tickets, g, W, lane,
+                                                     [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t srow = 0;
@@ -180,7 +181,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
     }
   }
   });
-  finish_chunks<DYN>(a.tickets, W, lane);
+  finish_parts<DYN ? kPartsClaimed : kPartsStatic>(a.tickets, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
   trace_wave(a.trace, a.trace_waves, g, t_start, lane);

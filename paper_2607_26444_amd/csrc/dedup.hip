@@ -112,7 +112,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
   const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
   uint32_t st = 0;
 
-  for_each_part<false>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
+  for_each_part<kPartsStatic>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
     s_last[wv][kWave + lane] = 0;
   }
 
-  for_each_part<false>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
+  for_each_part<kPartsStatic>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;

@@ -32,7 +32,7 @@ namespace {
 
 // VPL: 1 KiB segments held per lane-set (row bytes up to VPL KiB per pass).
 // FULL: row bytes == VPL KiB exactly (no per-lane tail test).
-template <int VPL, bool FULL, bool SCALES, bool DYN>
+template <int VPL, bool FULL, bool SCALES, int MODE>
 __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
   // Destination row (and scale row) of every slot of the current batch, one
   // entry per lane of each wavefront (0 = slot not dispatched), padded with
@@ -58,7 +58,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     if (SCALES) s_sdst[wv][kWave + lane] = 0;
   }
 
-  for_each_part<DYN>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
+  for_each_part<MODE>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t dst = 0, sdst = 0;
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     }
   }
   });
-  finish_chunks<DYN>(a.tickets, W, lane);
+  finish_parts<MODE>(a.tickets, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
   trace_wave(a.trace, a.trace_waves, g, t_start, lane);
@@ -248,8 +248,18 @@ hipError_t launch_pull(DispatchArgs a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int VPL, bool SCALES, bool DYN>
-hipError_t launch_push(DispatchArgs a, hipStream_t stream);
+template <int VPL, bool SCALES, int MODE>
+hipError_t launch_push_as(const DispatchArgs& a, int waves, bool full, hipStream_t stream) {
+  const dim3 grid(waves / kWavesPerBlock), block(kBlock);
+  if (full)
+    hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES, MODE>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((dispatch_kernel<VPL, false, SCALES, MODE>), grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int VPL, bool SCALES, int MODE>
+hipError_t launch_push(DispatchArgs a, hipStream_t stream, bool all_static = false);
 
 template <int VPL, bool SCALES>
 hipError_t launch_vpl(DispatchArgs a, int policy, hipStream_t stream) {
@@ -260,26 +270,25 @@ hipError_t launch_vpl(DispatchArgs a, int policy, hipStream_t stream) {
   if (policy == MOE_POLICY_BY_RANK)
     return full ? launch_pull<VPL, true, SCALES, MOE_POLICY_BY_RANK>(a, stream)
                 : launch_pull<VPL, false, SCALES, MOE_POLICY_BY_RANK>(a, stream);
-  if (policy == MOE_POLICY_DYNAMIC) return launch_push<VPL, SCALES, true>(a, stream);
-  return launch_push<VPL, SCALES, false>(a, stream);
+  if (policy == MOE_POLICY_DYNAMIC) return launch_push<VPL, SCALES, kPartsClaimed>(a, stream);
+  return launch_push<VPL, SCALES, kPartsHybrid>(a, stream, policy == MOE_POLICY_STATIC);
 }
 
-template <int VPL, bool SCALES, bool DYN>
-hipError_t launch_push(DispatchArgs a, hipStream_t stream) {
+template <int VPL, bool SCALES, int MODE>
+hipError_t launch_push(DispatchArgs a, hipStream_t stream, bool all_static) {
   const bool full = a.row_bytes == (int64_t)VPL * kWaveBytes;
   const void* fn =
-      full ? reinterpret_cast<const void*>(&dispatch_kernel<VPL, true, SCALES, DYN>)
-           : reinterpret_cast<const void*>(&dispatch_kernel<VPL, false, SCALES, DYN>);
+      full ? reinterpret_cast<const void*>(&dispatch_kernel<VPL, true, SCALES, MODE>)
+           : reinterpret_cast<const void*>(&dispatch_kernel<VPL, false, SCALES, MODE>);
   const int64_t rows = a.rows_hint > 0 ? a.rows_hint : a.k;
   const int waves = a.launch_waves > 0
                         ? a.launch_waves
                         : copy_waves(fn, rows * a.row_bytes, kDispatchInFlight, 256);
-  const dim3 grid(waves / kWavesPerBlock), block(kBlock);
-  if (full)
-    hipLaunchKernelGGL((dispatch_kernel<VPL, true, SCALES, DYN>), grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL((dispatch_kernel<VPL, false, SCALES, DYN>), grid, block, 0, stream, a);
-  return hipGetLastError();
+  // The run-time share pays one serialized counter claim per two parts; it
+  // only pays off while each wavefront owns several parts.
+  if (MODE == kPartsHybrid && (all_static || MOE_PLAN_PARTS / waves < 8))
+    return launch_push_as<VPL, SCALES, kPartsStatic>(a, waves, full, stream);
+  return launch_push_as<VPL, SCALES, MODE>(a, waves, full, stream);
 }
 
 template <bool SCALES>

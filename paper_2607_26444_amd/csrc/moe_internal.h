@@ -170,21 +170,23 @@ __device__ __forceinline__ float readlane_f32(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
-// Next unit of work for a wavefront.  Static: one contiguous run of plan
-// parts per wavefront.  Dynamic: a wavefront starts with part g and then
-// takes the next unclaimed part from a ticket counter (no waiting on other
-// wavefronts); the last wavefront to finish resets the counters for the next
-// launch.
-template <bool DYN>
-__device__ __forceinline__ int next_chunk(uint32_t* tickets, int W, int lane) {
-  int nxt = 0;
-  if (DYN && lane == 0) nxt = (int)atomicAdd(&tickets[0], 1u);
-  return W + __builtin_amdgcn_readfirstlane(nxt);
-}
+// How a copy kernel's wavefronts take the parts of the plan.
+//   kPartsStatic  wavefront g of W takes parts g, g + W, g + 2W, ...
+//   kPartsClaimed wavefront g takes part g, then claims the next unclaimed
+//                 part, one at a time, from a ticket counter in the workspace
+//   kPartsHybrid  the first half of the parts as kPartsStatic, the rest
+//                 claimed two at a time
+// Claimed parts come in plan order, so the wavefronts still sweep the tokens
+// as one front; claiming lets fast wavefronts take over the tail of slow
+// ones without waiting on anyone.  moe_layout zeroes the counters and the
+// last wavefront of a claiming launch resets them for the next one.
+constexpr int kPartsStatic = 0;
+constexpr int kPartsClaimed = 1;
+constexpr int kPartsHybrid = 2;
 
-template <bool DYN>
-__device__ __forceinline__ void finish_chunks(uint32_t* tickets, int W, int lane) {
-  if (DYN && lane == 0) {
+template <int MODE>
+__device__ __forceinline__ void finish_parts(uint32_t* tickets, int W, int lane) {
+  if (MODE != kPartsStatic && lane == 0) {
     if (atomicAdd(&tickets[1], 1u) == (uint32_t)(W - 1)) {
       tickets[0] = 0u;
       tickets[1] = 0u;
@@ -192,20 +194,18 @@ __device__ __forceinline__ void finish_chunks(uint32_t* tickets, int W, int lane
   }
 }
 
-// Visits the token range [t0, t1) of every plan part wavefront g owns.
-// Static: parts g, g + W, g + 2W, ...; their boundaries are fetched 64 at a
-// time, one part per lane, so stepping to the next part (often an empty one
-// when there are fewer tokens than parts) costs no global-memory round trip.
-// Dynamic: part g, then parts claimed from the ticket counter.
-template <bool DYN, typename F>
+// Calls body(t0, t1) for the token range of every part wavefront g of W
+// handles under MODE.  Part boundaries are fetched up to 64 at a time, one
+// part per lane, so stepping to the next part (often an empty one when there
+// are fewer tokens than parts) costs no global-memory round trip each.
+template <int MODE, typename F>
 __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* tickets, int g,
                                               int W, int lane, F&& body) {
-  if (DYN) {
-    for (int part = g; part < MOE_PLAN_PARTS; part = next_chunk<DYN>(tickets, W, lane))
-      body((int)ld4(bound + part), (int)ld4(bound + part + 1));
-    return;
-  }
-  const int m = (MOE_PLAN_PARTS - g + W - 1) / W;   // parts g + i*W < MOE_PLAN_PARTS
+  // static share: parts g + i*W below S
+  const int S = MODE == kPartsStatic   ? MOE_PLAN_PARTS
+                : MODE == kPartsHybrid ? (MOE_PLAN_PARTS / 2) / W * W
+                                       : (g < MOE_PLAN_PARTS ? g + 1 : g);
+  const int m = MODE == kPartsClaimed ? (g < MOE_PLAN_PARTS ? 1 : 0) : (S - g + W - 1) / W;
   for (int i0 = 0; i0 < m; i0 += kWave) {
     int b0 = 0, b1 = 0;
     if (i0 + lane < m) {
@@ -214,6 +214,24 @@ __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* ti
       b1 = (int)ld4(bound + part + 1);
     }
     const int n = m - i0 < kWave ? m - i0 : kWave;
+    for (int i = 0; i < n; ++i)
+      body(__builtin_amdgcn_readlane(b0, i), __builtin_amdgcn_readlane(b1, i));
+  }
+  if (MODE == kPartsStatic) return;
+  // claimed share: parts from `first` on, G per ticket
+  constexpr int G = MODE == kPartsHybrid ? 2 : 1;
+  const int first = MODE == kPartsHybrid ? S : W;
+  for (;;) {
+    int t = 0;
+    if (lane == 0) t = (int)atomicAdd(&tickets[0], 1u);
+    const int p0 = first + __builtin_amdgcn_readfirstlane(t) * G;
+    if (p0 >= MOE_PLAN_PARTS) break;
+    int b0 = 0, b1 = 0;
+    if (lane < G && p0 + lane < MOE_PLAN_PARTS) {
+      b0 = (int)ld4(bound + p0 + lane);
+      b1 = (int)ld4(bound + p0 + lane + 1);
+    }
+    const int n = MOE_PLAN_PARTS - p0 < G ? MOE_PLAN_PARTS - p0 : G;
     for (int i = 0; i < n; ++i)
       body(__builtin_amdgcn_readlane(b0, i), __builtin_amdgcn_readlane(b1, i));
   }

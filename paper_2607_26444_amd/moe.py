@@ -38,6 +38,7 @@ MOE_POLICY_BALANCED = 0
 MOE_POLICY_ROWS = 1
 MOE_POLICY_BY_RANK = 2
 MOE_POLICY_DYNAMIC = 3
+MOE_POLICY_STATIC = 4
 
 # Entry points declared in include/moe.h.
 EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error", "moe_wall_clock_khz",

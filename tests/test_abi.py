@@ -39,7 +39,7 @@ def test_binding_covers_every_declared_symbol():
 
 
 def test_version_and_strerror():
-    assert moe.moe_version() == 3
+    assert moe.moe_version() == 4
     for code in (0, -1, -2, -3, -4, -99):
         assert isinstance(moe.lib().moe_strerror(code), bytes)
 
@@ -95,7 +95,7 @@ def _dispatch_args(**kw):
 def test_dispatch_argument_errors():
     L = moe.lib()
     assert L.moe_dispatch_ex(*_dispatch_args(dtype=7)) == moe.MOE_EINVAL
-    assert L.moe_dispatch_ex(*_dispatch_args(policy=4)) == moe.MOE_EINVAL
+    assert L.moe_dispatch_ex(*_dispatch_args(policy=5)) == moe.MOE_EINVAL
     assert L.moe_dispatch_ex(*_dispatch_args(policy=1, rs=None)) == moe.MOE_EINVAL
     assert L.moe_dispatch_ex(*_dispatch_args(x=MIS)) == moe.MOE_EALIGN
     assert L.moe_dispatch_ex(*_dispatch_args(H=7164)) == moe.MOE_EALIGN      # 2H % 16

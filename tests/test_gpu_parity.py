@@ -167,9 +167,11 @@ def test_dynamic_policy_matches_oracle(T, H, E, R, k, payload, mask):
     inp = wl.make_inputs(cfg)
     idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
     _full_parity(cfg, inp, idx=idx, policy=3, combine_policy=3, repeat=3)
+    # the default split hands out its second half at run time: same reset
+    _full_parity(cfg, inp, idx=idx, policy=0, combine_policy=0, repeat=3)
 
 
-@pytest.mark.parametrize("policy,cpolicy", [(0, 0), (1, 0), (2, 0), (3, 3)])
+@pytest.mark.parametrize("policy,cpolicy", [(0, 0), (1, 0), (2, 0), (3, 3), (4, 4)])
 @pytest.mark.parametrize("waves", [64, 256, 3072])
 def test_explicit_wave_counts_match_oracle(policy, cpolicy, waves):
     """Every work split gives the oracle's bytes and y at a chosen wavefront
