@@ -432,6 +432,8 @@ int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype,
   a.tok_pos = tok_pos;
   a.tok_offset = tok_offset;
   a.bound = static_cast<const int32_t*>(workspace);
+  a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
+                                          moe::layout_geom(T, E).ticket_offset) + 4;
   a.status = status;
   return launched(moe::launch_expand(a, as_stream(stream)));
 }

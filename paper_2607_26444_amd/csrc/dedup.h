@@ -44,6 +44,7 @@ struct ExpandArgs {
   const int32_t* tok_pos;
   const int32_t* tok_offset;
   const int32_t* bound;          // plan of the per-slot layout
+  uint32_t* tickets;             // claimed parts: {next, done}, zeroed by the layout
   uint32_t* status;
 };
 

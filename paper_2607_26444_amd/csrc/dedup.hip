@@ -88,7 +88,8 @@ __device__ __forceinline__ void order_slot(const int* key, const int* q, int bas
 }
 
 // VPL: 1 KiB segments held per lane-set; FULL: row bytes == VPL KiB.
-template <int VPL, bool FULL, bool SCALES>
+// MODE: how the wavefronts take the plan's parts (as dispatch).
+template <int VPL, bool FULL, bool SCALES, int MODE>
 __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
   __shared__ int s_key[kWavesPerBlock][kWave];
   __shared__ int s_q[kWavesPerBlock][kWave];
@@ -112,7 +113,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
   const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
   uint32_t st = 0;
 
-  for_each_part<kPartsStatic>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
+  for_each_part<MODE>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -211,6 +212,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
     }
   }
   });
+  finish_parts<MODE>(a.tickets, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
 }
@@ -415,21 +417,30 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
   if (st && lane == 0) atomicOr(a.status, st);
 }
 
+template <int VPL, bool SCALES, int MODE>
+hipError_t launch_expand_as(const ExpandArgs& a, int waves, bool full, hipStream_t stream) {
+  const dim3 grid(waves / kWavesPerBlock), block(kBlock);
+  if (full)
+    hipLaunchKernelGGL((expand_kernel<VPL, true, SCALES, MODE>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((expand_kernel<VPL, false, SCALES, MODE>), grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
 template <int VPL, bool SCALES>
 hipError_t launch_expand_vpl(ExpandArgs a, hipStream_t stream) {
   const bool full = a.row_bytes == (int64_t)VPL * kWaveBytes;
-  const void* fn = full ? reinterpret_cast<const void*>(&expand_kernel<VPL, true, SCALES>)
-                        : reinterpret_cast<const void*>(&expand_kernel<VPL, false, SCALES>);
+  const void* fn =
+      full ? reinterpret_cast<const void*>(&expand_kernel<VPL, true, SCALES, kPartsHybrid>)
+           : reinterpret_cast<const void*>(&expand_kernel<VPL, false, SCALES, kPartsHybrid>);
   // a token's pair rows are loaded one after another: about half of
   // dispatch's stores are in flight per wavefront
   const int waves =
       copy_waves(fn, (int64_t)(a.k + 1) / 2 * a.row_bytes, kDispatchInFlight, 256);
-  const dim3 grid(waves / kWavesPerBlock), block(kBlock);
-  if (full)
-    hipLaunchKernelGGL((expand_kernel<VPL, true, SCALES>), grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL((expand_kernel<VPL, false, SCALES>), grid, block, 0, stream, a);
-  return hipGetLastError();
+  // as dispatch: the claimed half only while a wavefront owns several parts
+  if (MOE_PLAN_PARTS / waves < 8)
+    return launch_expand_as<VPL, SCALES, kPartsStatic>(a, waves, full, stream);
+  return launch_expand_as<VPL, SCALES, kPartsHybrid>(a, waves, full, stream);
 }
 
 template <bool SCALES>

@@ -244,7 +244,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       rank_offset[R] = FIXED ? E * C : (int32_t)n_total;
       bound[0] = 0;
     }
-    if (tid < 4) tickets[tid] = 0u;  // work tickets of dispatch and combine
+    if (tid < 8) tickets[tid] = 0u;  // work tickets of dispatch, combine, expand
     for (int r = tid; r < R; r += kBlock) {
       rank_offset[r] = FIXED ? r * L * C : eoff[r * L];
       rank_count[r] = eoff[(r + 1) * L] - eoff[r * L];

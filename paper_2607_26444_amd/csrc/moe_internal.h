@@ -27,7 +27,7 @@ struct LayoutGeom {
   int nc;
   int ncp;              // nc rounded up to a multiple of 4
   size_t plan_bytes;    // bound[MOE_PLAN_PARTS + 1], padded to 256 bytes
-  size_t ticket_offset; // 4 uint32 work tickets (dispatch next/done, combine next/done)
+  size_t ticket_offset; // 8 uint32 work tickets ({next, done} of dispatch, combine, expand)
   size_t counts_offset;
   size_t counts_bytes;  // int32 [E][ncp], expert-major
   size_t total;
