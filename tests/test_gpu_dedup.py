@@ -71,6 +71,7 @@ def oracle_plan(tok_pos, T, k):
     (1000, 1032, 24, 6, 3, wl.BF16, 0.1, 0.0),
     (700, 640, 32, 8, 5, wl.FP8_E4M3, 0.05, 0.0),
     (2049, 7168, 256, 64, 8, wl.BF16, 0.0, 1.2),
+    (400, 6152, 64, 16, 8, wl.BF16, 0.1, 1.2),     # 12 KiB + 16 B source-sum rows
     (513, 4096, 128, 32, 8, wl.FP8_E4M3, 0.0, 1.2),
     (300, 256, 16, 4, 1, wl.BF16, 0.0, 0.0),       # k = 1: every slot is a pair
     (200, 512, 16, 16, 4, wl.BF16, 0.0, 0.0),      # one expert per peer

@@ -119,6 +119,28 @@ def test_custom_shapes(T, H, E, R, k, payload, mask):
     _full_parity(cfg, inp, idx=idx)
 
 
+@pytest.mark.parametrize("T,H,E,R,k,mask,cap", [
+    (300, 4104, 32, 8, 2, 0.1, False),    # 8 KiB + 16 B: one lane in the last segment
+    (257, 6152, 64, 16, 4, 0.2, True),    # 12 KiB + 16 B, capacity drops
+    (129, 7176, 256, 64, 7, 0.05, False),  # slot width 8 with one pad slot, ragged tail
+    (200, 8192, 64, 16, 8, 0.1, True),    # 16 KiB: every register segment used
+    (200, 4096, 64, 16, 8, 0.1, False),   # 8 KiB: segment-by-segment path, just below
+    (200, 8200, 64, 16, 8, 0.1, False),   # 16 KiB + 16 B: segment-by-segment, just above
+])
+def test_combine_row_widths(T, H, E, R, k, mask, cap):
+    """Combine output rows around the widths that are reduced into registers
+    and stored as one burst (more than 8, at most 16 KiB): ragged last
+    segments, masked and capacity-dropped slots, both neighbours."""
+    cfg = wl.custom(T, H, E, R, k, zipf_s=1.2, seed=T + H + k)
+    inp = wl.make_inputs(cfg)
+    idx = wl.mask_slots(inp["topk_idx"], mask, seed=T) if mask else None
+    delta = None
+    if cap:
+        delta = [0] * R
+        delta[0] = -7
+    _full_parity(cfg, inp, idx=idx, cap_delta=delta, spare_rows=1)
+
+
 @pytest.mark.parametrize("pitch", [0, 116, 128, 256])
 def test_fp8_scale_pitch(pitch):
     """Scale rows (112 bytes here) packed (pitch 0) or pitched: scales then
