@@ -16,9 +16,9 @@
 // [e*C, (e+1)*C) instead of after the previous experts' rows.
 //
 //   layout_place  every chunk reads the whole count matrix (small by
-//                 construction, stored expert-major), derives the global
+//                 construction, stored chunk-major), derives the global
 //                 per-expert totals, their exclusive scan (expert_offset) and
-//                 its own column prefix,
+//                 its own prefix over earlier chunks,
 //                 then rebuilds its bitmaps and gives each routed slot
 //                     pos = expert_offset[e] + (rows of e in earlier chunks)
 //                         + (rows of e in earlier sub-chunks of this chunk)
@@ -123,12 +123,14 @@ __global__ __launch_bounds__(kBlock) void layout_count_kernel(
     }
     __syncthreads();
   }
-  for (int e = tid; e < E; e += kBlock) counts[(int64_t)e * ncp + blockIdx.x] = cnt[e];
+  for (int e = tid; e < E; e += kBlock) counts[(int64_t)blockIdx.x * ncp + e] = cnt[e];
   st = wave_or(st);
   if (lane == 0 && st) atomicOr(status, st);
 }
 
 constexpr int kMaxExpertsPerThread = MOE_MAX_EXPERTS / kBlock;  // 4
+constexpr int kCountBatch = 16;      // 16-byte count loads in flight per thread
+constexpr int kMaxCountGroups = 16;  // count-matrix rows read side by side
 
 // SINGLE: the whole batch is one sub-chunk (T <= kBlock), so this kernel
 // also does the counting (no layout_count launch): the totals are the
@@ -148,6 +150,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   int64_t* scan = reinterpret_cast<int64_t*>(mask + kWavesPerBlock * E);  // [4]
   int32_t* base = reinterpret_cast<int32_t*>(scan + kWavesPerBlock);  // [E]
   int32_t* eoff = base + E;                                         // [E+1]
+  int32_t* woff = eoff + E + 1;  // [4][E]; before placement, 2 x [groups][ncp] count partials
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const int c = blockIdx.x;
@@ -183,25 +186,53 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
         for (int ww = 0; ww < kWavesPerBlock; ++ww) tot[q] += __popcll(mask[ww * E + e]);
     }
   } else {
-    // The count matrix is expert-major ([E][ncp], ncp = nc rounded up to 4),
-    // so an expert's column is contiguous and arrives in independent 16-byte
-    // loads that are all in flight together.
+    // The count matrix is chunk-major ([nc][ncp], row pitch ncp = E rounded
+    // up to 4).  Lanes read neighbouring 16-byte groups of one chunk's row
+    // (coalesced), `groups` rows are read side by side, and each thread adds
+    // its four experts over every groups-th row with a batch of loads in
+    // flight before the first is used.  The groups' partial sums meet in LDS.
+    const int q4 = ncp / 4;
+    const int groups = min(kBlock / q4, kMaxCountGroups);
+    const int gi = tid / q4, li = tid - gi * q4;
+    int32_t* part_t = woff;                   // [groups][ncp], free until placement
+    int32_t* part_p = woff + groups * ncp;
+    if (gi < groups) {
+      int4 ta = {0, 0, 0, 0}, pa = {0, 0, 0, 0};
+      for (int r0 = gi; r0 < nc; r0 += groups * kCountBatch) {
+        int4 v[kCountBatch];
+#pragma unroll
+        for (int u = 0; u < kCountBatch; ++u) {
+          const int r = min(r0 + u * groups, nc - 1);  // past nc: re-read, ignored
+          v[u] = reinterpret_cast<const int4*>(counts + (int64_t)r * ncp)[li];
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep every load ahead of the first use
+#pragma unroll
+        for (int u = 0; u < kCountBatch; ++u) {
+          const int r = r0 + u * groups;
+          const int in = r < nc ? 1 : 0, before = r < c ? 1 : 0;
+          ta.x += in * v[u].x;
+          ta.y += in * v[u].y;
+          ta.z += in * v[u].z;
+          ta.w += in * v[u].w;
+          pa.x += before * v[u].x;
+          pa.y += before * v[u].y;
+          pa.z += before * v[u].z;
+          pa.w += before * v[u].w;
+        }
+      }
+      reinterpret_cast<int4*>(part_t + gi * ncp)[li] = ta;
+      reinterpret_cast<int4*>(part_p + gi * ncp)[li] = pa;
+    }
+    __syncthreads();
 #pragma unroll
     for (int q = 0; q < kMaxExpertsPerThread; ++q) {
       tot[q] = pre[q] = 0;
       const int e = tid * ept + q;
-      if (q < ept && e < E) {
-        const int4* col = reinterpret_cast<const int4*>(counts + (int64_t)e * ncp);
-#pragma unroll 8
-        for (int i = 0; i < ncp / 4; ++i) {
-          const int4 v = col[i];
-          const int cc = 4 * i;
-          tot[q] += (cc < nc ? v.x : 0) + (cc + 1 < nc ? v.y : 0) + (cc + 2 < nc ? v.z : 0) +
-                    (cc + 3 < nc ? v.w : 0);
-          pre[q] += (cc < c ? v.x : 0) + (cc + 1 < c ? v.y : 0) + (cc + 2 < c ? v.z : 0) +
-                    (cc + 3 < c ? v.w : 0);
+      if (q < ept && e < E)
+        for (int g = 0; g < groups; ++g) {
+          tot[q] += part_t[g * ncp + e];
+          pre[q] += part_p[g * ncp + e];
         }
-      }
     }
   }
   // Rows each expert gets: all of its slots, or at most C in fixed windows.
@@ -277,6 +308,20 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
         if (ok[j]) atomicOr(&mask[w * E + ev[j]], 1ull << lane);
       __syncthreads();
     }
+    // woff[q][e]: first row of expert e for wavefront q of this sub-chunk
+    // (base plus the rows of e in wavefronts 0..q-1); base moves past the
+    // sub-chunk.  A slot's row is then one lookup plus its rank in its own
+    // wavefront's bitmap.
+    for (int e = tid; e < E; e += kBlock) {
+      int r = base[e];
+#pragma unroll
+      for (int q = 0; q < kWavesPerBlock; ++q) {
+        woff[q * E + e] = r;
+        r += __popcll(mask[q * E + e]);
+      }
+      base[e] = r;
+    }
+    __syncthreads();
     const uint64_t below = (1ull << lane) - 1ull;
     int nplaced = 0;
 #pragma unroll
@@ -285,8 +330,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
         int p = -1;
         if (ok[j]) {
           const int e = ev[j];
-          int r = base[e] + __popcll(mask[w * E + e] & below);
-          for (int q = 0; q < w; ++q) r += __popcll(mask[q * E + e]);
+          const int r = woff[w * E + e] + __popcll(mask[w * E + e] & below);
           if (!FIXED || r - e * C < C) {
             p = r;
             row_src[p] = (int32_t)(t * k + j);
@@ -309,15 +353,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     }
     cost_base += sub_total;
     __syncthreads();
-    for (int e = tid; e < E; e += kBlock) {
-      int n = 0;
-#pragma unroll
-      for (int q = 0; q < kWavesPerBlock; ++q) {
-        n += __popcll(mask[q * E + e]);
-        mask[q * E + e] = 0;
-      }
-      base[e] += n;
-    }
+    for (int i = tid; i < kWavesPerBlock * E; i += kBlock) mask[i] = 0;
     __syncthreads();
   }
 
@@ -348,8 +384,12 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R, 
   int32_t* counts = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + g.counts_offset);
   uint32_t* tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + g.ticket_offset);
   const size_t lds_count = (size_t)kWavesPerBlock * E * 8 + (size_t)E * 4;
+  // woff also holds the two [groups][ncp] count partials (groups * ncp <=
+  // 4 * kBlock int32 each) before placement starts.
+  const size_t woff_ints = (size_t)kWavesPerBlock * E > 8 * kBlock ? (size_t)kWavesPerBlock * E
+                                                                    : 8 * kBlock;
   const size_t lds_place = (size_t)kWavesPerBlock * E * 8 + kWavesPerBlock * 8 +
-                           (size_t)E * 4 + (size_t)(E + 1) * 4;
+                           (size_t)E * 4 + (size_t)(E + 1) * 4 + woff_ints * 4;
   if (g.nc == 1 && T <= kBlock) {
     hipLaunchKernelGGL((layout_place_kernel<KW, true, FIXED>), dim3(1), dim3(kBlock), lds_place,
                        stream, idx, T, k, E, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
@@ -380,11 +420,11 @@ LayoutGeom layout_geom(int64_t T, int E) {
   g.chunk_tokens = kBlock * (per < 1 ? 1 : per);
   g.nc = (int)((T + g.chunk_tokens - 1) / g.chunk_tokens);
   if (g.nc < 1) g.nc = 1;
-  g.ncp = (g.nc + 3) / 4 * 4;
+  g.ncp = (E + 3) / 4 * 4;
   g.plan_bytes = ((size_t)(MOE_PLAN_PARTS + 1) * 4 + 255) / 256 * 256;
   g.ticket_offset = g.plan_bytes;
   g.counts_offset = g.ticket_offset + 256;
-  g.counts_bytes = (size_t)g.ncp * E * 4;
+  g.counts_bytes = (size_t)g.nc * g.ncp * 4;
   g.total = g.counts_offset + (g.counts_bytes + 255) / 256 * 256;
   return g;
 }

@@ -25,11 +25,11 @@ constexpr int kMaxSegVecs = 16;      // a wavefront holds up to 16 KiB of a row
 struct LayoutGeom {
   int64_t chunk_tokens;
   int nc;
-  int ncp;              // nc rounded up to a multiple of 4
+  int ncp;              // row pitch of the count matrix: E rounded up to 4
   size_t plan_bytes;    // bound[MOE_PLAN_PARTS + 1], padded to 256 bytes
   size_t ticket_offset; // 8 uint32 work tickets ({next, done} of dispatch, combine, expand)
   size_t counts_offset;
-  size_t counts_bytes;  // int32 [E][ncp], expert-major
+  size_t counts_bytes;  // int32 [nc][ncp], chunk-major
   size_t total;
 };
 
