@@ -203,6 +203,16 @@ def test_explicit_wave_counts_match_oracle(policy, cpolicy, waves):
     _full_parity(cfg, policy=policy, combine_policy=cpolicy, waves=waves, repeat=2)
 
 
+@pytest.mark.parametrize("cpolicy,waves", [(0, 64), (0, 3072), (3, 256), (3, 3072)])
+def test_combine_burst_rows_at_explicit_wave_counts(cpolicy, waves):
+    """12 KiB output rows (stored from registers) under both combine splits,
+    with fewer wavefronts than CUs and more than fit on the device at once."""
+    cfg = wl.custom(1500, 6144, 64, 16, 8, zipf_s=1.2, seed=waves + cpolicy)
+    inp = wl.make_inputs(cfg)
+    idx = wl.mask_slots(inp["topk_idx"], 0.05, seed=waves)
+    _full_parity(cfg, inp, idx=idx, combine_policy=cpolicy, waves=waves, repeat=2)
+
+
 @pytest.mark.parametrize("T,H,E,R,k,payload,C,zipf", [
     (1000, 1032, 24, 6, 3, wl.BF16, 200, 0.0),      # ample windows
     (1000, 1032, 24, 6, 3, wl.BF16, 60, 1.2),       # hot experts overflow
