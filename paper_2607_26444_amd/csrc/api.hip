@@ -363,17 +363,12 @@ int moe_layout_dedup(const int32_t* topk_idx, int64_t T, int k, int E, int R, in
   if (T > 0 && (!topk_idx || !tok_pos || !tok_src)) return MOE_EINVAL;
   const moe::DedupGeom d = moe::dedup_geom(T, k, R);
   if (!aligned(workspace, 256) || workspace_bytes < d.total) return MOE_EWORKSPACE;
-  char* ws = static_cast<char*>(workspace);
-  int32_t* rank_idx = reinterpret_cast<int32_t*>(ws + d.rank_idx_offset);
-  int32_t* spare = reinterpret_cast<int32_t*>(ws + d.spare_offset);
-  hipError_t err = hipSuccess;
-  if (T > 0) err = moe::launch_rank_index(topk_idx, T, k, E, E / R, rank_idx, status,
-                                          as_stream(stream));
-  if (err != hipSuccess) return launched(err);
-  // the layout pass over peers: one "expert" per peer, one peer per "rank"
-  return launched(moe::launch_layout(rank_idx, T, k, R, R, -1, tok_count, tok_offset, spare,
+  int32_t* spare = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + d.spare_offset);
+  // the layout pass over peers: one "expert" per peer, one peer per "rank",
+  // the expert indices binned by peer as they are read
+  return launched(moe::launch_layout(topk_idx, T, k, R, R, -1, tok_count, tok_offset, spare,
                                      spare + R, tok_pos, tok_src, workspace, status,
-                                     as_stream(stream)));
+                                     as_stream(stream), E / R));
 }
 
 int moe_dispatch_dedup(const void* x, const float* x_scales, int dtype, int64_t T, int H, int k,

@@ -10,21 +10,15 @@
 namespace moe {
 
 // Layout of the workspace of moe_layout_dedup: the layout pass over peers
-// (plan first, as every copy kernel expects), then the peer index of every
-// slot and the two arrays the layout pass writes but the caller does not see.
+// (plan first, as every copy kernel expects), then the two arrays the layout
+// pass writes but the caller does not see.
 struct DedupGeom {
   LayoutGeom g;          // layout_geom(T, R)
-  size_t rank_idx_offset;
   size_t spare_offset;   // int32 [R] + int32 [R + 1]
   size_t total;
 };
 
 DedupGeom dedup_geom(int64_t T, int k, int R);
-
-// rank_idx[t,j] = e/L for the first routed slot of token t with an expert on
-// peer e/L, -1 for every other slot; status bits 1 and 2 as in the layout.
-hipError_t launch_rank_index(const int32_t* topk_idx, int64_t T, int k, int E, int L,
-                             int32_t* rank_idx, uint32_t* status, hipStream_t stream);
 
 struct ExpandArgs {
   const uint64_t* dedup_x;       // [R] pair-row region bases

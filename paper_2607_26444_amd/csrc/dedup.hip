@@ -6,9 +6,9 @@
 // peer that Section 6.2 balances shrinks by the duplicates):
 //
 //   moe_layout_dedup   one row per (token, peer) pair, token order per peer
-//                      (the layout kernels run over a peer index of every
-//                      slot: the peer of the token's first slot on it, -1
-//                      for the token's other slots on the same peer);
+//                      (the layout kernels over peers: each slot reads as
+//                      its peer if it is the token's first slot on it, as
+//                      unrouted otherwise);
 //   moe_dispatch_dedup the dispatch kernel over the pair rows;
 //   moe_expand         on the receiving peer: pair rows -> expert-ordered
 //                      rows, the layout a per-slot dispatch would have left;
@@ -30,39 +30,6 @@ namespace moe {
 namespace {
 
 constexpr int kNoKey = 0x7FFFFFFF;   // sort key of an unrouted slot (last)
-
-template <int KW>
-__global__ __launch_bounds__(kBlock) void rank_index_kernel(const int32_t* __restrict__ topk_idx,
-                                                            int64_t T, int k, int E, int L,
-                                                            int32_t* __restrict__ rank_idx,
-                                                            uint32_t* status) {
-  const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  uint32_t st = 0;
-  if (t < T) {
-    int e[KW];
-    bool used[KW];
-#pragma unroll
-    for (int j = 0; j < KW; ++j) e[j] = j < k ? topk_idx[t * k + j] : -1;
-#pragma unroll
-    for (int j = 0; j < KW; ++j) {
-      const bool bad = e[j] < -1 || e[j] >= E;
-      bool rep = false;
-#pragma unroll
-      for (int jj = 0; jj < j; ++jj) rep = rep || e[jj] == e[j];
-      const bool ok = e[j] >= 0 && !bad;
-      st |= bad ? MOE_STATUS_BAD_INDEX : 0u;
-      st |= (ok && rep) ? MOE_STATUS_DUP_INDEX : 0u;
-      used[j] = ok && !rep;
-      const int r = used[j] ? e[j] / L : -1;
-      bool seen = false;
-#pragma unroll
-      for (int jj = 0; jj < j; ++jj) seen = seen || (used[jj] && e[jj] / L == r);
-      if (j < k) rank_idx[t * k + j] = (used[j] && !seen) ? r : -1;
-    }
-  }
-  st = wave_or(st);
-  if (st && (threadIdx.x & (kWave - 1)) == 0) atomicOr(status, st);
-}
 
 // Position of slot lj of a token after ordering the token's k slots by
 // (key, slot), whether it opens or closes its run of equal keys, and the
@@ -476,35 +443,14 @@ hipError_t launch_local_kw(LocalArgs a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int KW>
-hipError_t launch_rank_index_kw(const int32_t* topk_idx, int64_t T, int k, int E, int L,
-                                int32_t* rank_idx, uint32_t* status, hipStream_t stream) {
-  const int64_t blocks = (T + kBlock - 1) / kBlock;
-  hipLaunchKernelGGL((rank_index_kernel<KW>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                     topk_idx, T, k, E, L, rank_idx, status);
-  return hipGetLastError();
-}
-
 }  // namespace
 
 DedupGeom dedup_geom(int64_t T, int k, int R) {
   DedupGeom d;
   d.g = layout_geom(T, R);
-  d.rank_idx_offset = (d.g.total + 255) / 256 * 256;
-  d.spare_offset = d.rank_idx_offset + ((size_t)T * k * 4 + 255) / 256 * 256;
+  d.spare_offset = (d.g.total + 255) / 256 * 256;
   d.total = d.spare_offset + ((size_t)(2 * R + 1) * 4 + 255) / 256 * 256;
   return d;
-}
-
-hipError_t launch_rank_index(const int32_t* topk_idx, int64_t T, int k, int E, int L,
-                             int32_t* rank_idx, uint32_t* status, hipStream_t stream) {
-  switch (slot_width(k)) {
-    case 2: return launch_rank_index_kw<2>(topk_idx, T, k, E, L, rank_idx, status, stream);
-    case 4: return launch_rank_index_kw<4>(topk_idx, T, k, E, L, rank_idx, status, stream);
-    case 8: return launch_rank_index_kw<8>(topk_idx, T, k, E, L, rank_idx, status, stream);
-    case 16: return launch_rank_index_kw<16>(topk_idx, T, k, E, L, rank_idx, status, stream);
-    default: return launch_rank_index_kw<32>(topk_idx, T, k, E, L, rank_idx, status, stream);
-  }
 }
 
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {

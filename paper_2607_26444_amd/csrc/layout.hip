@@ -30,7 +30,9 @@
 //                 boundaries that fall inside the chunk.
 //
 // Both kernels decide slot validity with the same routine (load_row), so
-// counts and positions always agree.
+// counts and positions always agree.  With peer_L > 0 the same kernels lay
+// out one row per (token, peer) pair: E is then the number of peers and
+// load_row bins the expert indices by peer as it reads them.
 
 #include "moe_internal.h"
 
@@ -39,9 +41,12 @@ namespace {
 
 // Load token t's k expert indices and decide which slots are routed: an
 // index in [0, E) that does not repeat an earlier slot of the row.
+// L > 0 (per-peer layout): the indices are experts in [0, E*L), L per peer,
+// and each slot becomes its peer e / L if it is the row's first routed slot
+// on that peer, else unrouted; the status bits still judge the experts.
 template <int KW>
 __device__ __forceinline__ void load_row(const int32_t* __restrict__ idx, int64_t t, int64_t T,
-                                         int k, int E, int (&ev)[KW], bool (&ok)[KW],
+                                         int k, int E, int L, int (&ev)[KW], bool (&ok)[KW],
                                          uint32_t& st) {
 #pragma unroll
   for (int j = 0; j < KW; ++j) ev[j] = -1;
@@ -50,16 +55,30 @@ __device__ __forceinline__ void load_row(const int32_t* __restrict__ idx, int64_
     for (int j = 0; j < KW; ++j)
       if (j < k) ev[j] = idx[t * k + j];
   }
+  const int n = L > 0 ? E * L : E;
 #pragma unroll
   for (int j = 0; j < KW; ++j) {
     const int e = ev[j];
-    const bool in_range = e >= 0 && e < E;
-    if (e < -1 || e >= E) st |= MOE_STATUS_BAD_INDEX;
+    const bool in_range = e >= 0 && e < n;
+    if (e < -1 || e >= n) st |= MOE_STATUS_BAD_INDEX;
     bool repeat = false;
 #pragma unroll
     for (int jj = 0; jj < j; ++jj) repeat |= (ev[jj] == e);
     if (in_range && repeat) st |= MOE_STATUS_DUP_INDEX;
     ok[j] = in_range && !repeat;
+  }
+  if (L > 0) {
+    int pr[KW];
+#pragma unroll
+    for (int j = 0; j < KW; ++j) pr[j] = ok[j] ? ev[j] / L : -1;
+#pragma unroll
+    for (int j = 0; j < KW; ++j) {
+      bool seen = false;
+#pragma unroll
+      for (int jj = 0; jj < j; ++jj) seen |= (ok[jj] && pr[jj] == pr[j]);
+      ev[j] = pr[j];
+      ok[j] = ok[j] && !seen;
+    }
   }
 }
 
@@ -90,8 +109,8 @@ __device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* scra
 
 template <int KW>
 __global__ __launch_bounds__(kBlock) void layout_count_kernel(
-    const int32_t* __restrict__ idx, int64_t T, int k, int E, int64_t chunk_tokens, int ncp,
-    int32_t* __restrict__ counts, uint32_t* __restrict__ status) {
+    const int32_t* __restrict__ idx, int64_t T, int k, int E, int peer_L, int64_t chunk_tokens,
+    int ncp, int32_t* __restrict__ counts, uint32_t* __restrict__ status) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* mask = reinterpret_cast<uint64_t*>(smem);           // [4][E]
   int32_t* cnt = reinterpret_cast<int32_t*>(mask + kWavesPerBlock * E);  // [E]
@@ -107,7 +126,7 @@ __global__ __launch_bounds__(kBlock) void layout_count_kernel(
   for (int64_t s0 = c0; s0 < c1; s0 += kBlock) {
     int ev[KW];
     bool ok[KW];
-    load_row<KW>(idx, s0 + tid, c1, k, E, ev, ok, st);
+    load_row<KW>(idx, s0 + tid, c1, k, E, peer_L, ev, ok, st);
 #pragma unroll
     for (int j = 0; j < KW; ++j)
       if (ok[j]) atomicOr(&mask[w * E + ev[j]], 1ull << lane);
@@ -139,8 +158,8 @@ constexpr int kMaxCountGroups = 16;  // count-matrix rows read side by side
 // starts at e*C); a slot whose rank within its expert reaches C is dropped.
 template <int KW, bool SINGLE, bool FIXED>
 __global__ __launch_bounds__(kBlock) void layout_place_kernel(
-    const int32_t* __restrict__ idx, int64_t T, int k, int E, int R, int C, int64_t chunk_tokens,
-    int nc, int ncp, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
+    const int32_t* __restrict__ idx, int64_t T, int k, int E, int peer_L, int R, int C,
+    int64_t chunk_tokens, int nc, int ncp, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
     int32_t* __restrict__ expert_offset, int32_t* __restrict__ rank_count,
     int32_t* __restrict__ rank_offset, int32_t* __restrict__ pos,
     int32_t* __restrict__ row_src, int32_t* __restrict__ bound, uint32_t* __restrict__ tickets,
@@ -165,7 +184,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   int ev0[KW];
   bool ok0[KW];
   uint32_t st = 0;
-  load_row<KW>(idx, c0 + tid, c1, k, E, ev0, ok0, st);
+  load_row<KW>(idx, c0 + tid, c1, k, E, peer_L, ev0, ok0, st);
 
   // Totals and this chunk's prefix for the experts this thread owns:
   // e = tid*EPT .. tid*EPT+EPT-1 (contiguous, so a scan over threads is a
@@ -300,7 +319,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       }
     } else {
       uint32_t st_more = 0;
-      load_row<KW>(idx, t, c1, k, E, ev, ok, st_more);
+      load_row<KW>(idx, t, c1, k, E, peer_L, ev, ok, st_more);
     }
     if (!SINGLE) {
 #pragma unroll
@@ -374,7 +393,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
 }
 
 template <int KW, bool FIXED>
-hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R, int C,
+hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int peer_L, int R, int C,
                             int32_t* expert_count, int32_t* expert_offset,
                             int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
                             int32_t* row_src, void* workspace, uint32_t* status,
@@ -392,18 +411,18 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int R, 
                            (size_t)E * 4 + (size_t)(E + 1) * 4 + woff_ints * 4;
   if (g.nc == 1 && T <= kBlock) {
     hipLaunchKernelGGL((layout_place_kernel<KW, true, FIXED>), dim3(1), dim3(kBlock), lds_place,
-                       stream, idx, T, k, E, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
+                       stream, idx, T, k, E, peer_L, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
                        expert_count,
                        expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
                        status);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(layout_count_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_count, stream,
-                     idx, T, k, E, g.chunk_tokens, g.ncp, counts, status);
+                     idx, T, k, E, peer_L, g.chunk_tokens, g.ncp, counts, status);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL((layout_place_kernel<KW, false, FIXED>), dim3(g.nc), dim3(kBlock),
-                     lds_place, stream, idx, T, k, E, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
+                     lds_place, stream, idx, T, k, E, peer_L, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
                      expert_count,
                      expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
                      status);
@@ -436,29 +455,29 @@ int slot_width(int k) {
 }
 
 template <bool FIXED>
-hipError_t launch_layout_fx(const int32_t* idx, int64_t T, int k, int E, int R, int C,
+hipError_t launch_layout_fx(const int32_t* idx, int64_t T, int k, int E, int peer_L, int R, int C,
                             int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
                             int32_t* rank_offset, int32_t* pos, int32_t* row_src,
                             void* workspace, uint32_t* status, hipStream_t stream) {
   switch (slot_width(k)) {
     case 2:
-      return launch_layout_kw<2, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+      return launch_layout_kw<2, FIXED>(idx, T, k, E, peer_L, R, C, expert_count, expert_offset,
                                         rank_count, rank_offset, pos, row_src, workspace,
                                         status, stream);
     case 4:
-      return launch_layout_kw<4, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+      return launch_layout_kw<4, FIXED>(idx, T, k, E, peer_L, R, C, expert_count, expert_offset,
                                         rank_count, rank_offset, pos, row_src, workspace,
                                         status, stream);
     case 8:
-      return launch_layout_kw<8, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+      return launch_layout_kw<8, FIXED>(idx, T, k, E, peer_L, R, C, expert_count, expert_offset,
                                         rank_count, rank_offset, pos, row_src, workspace,
                                         status, stream);
     case 16:
-      return launch_layout_kw<16, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+      return launch_layout_kw<16, FIXED>(idx, T, k, E, peer_L, R, C, expert_count, expert_offset,
                                          rank_count, rank_offset, pos, row_src, workspace,
                                          status, stream);
     default:
-      return launch_layout_kw<32, FIXED>(idx, T, k, E, R, C, expert_count, expert_offset,
+      return launch_layout_kw<32, FIXED>(idx, T, k, E, peer_L, R, C, expert_count, expert_offset,
                                          rank_count, rank_offset, pos, row_src, workspace,
                                          status, stream);
   }
@@ -467,13 +486,13 @@ hipError_t launch_layout_fx(const int32_t* idx, int64_t T, int k, int E, int R, 
 hipError_t launch_layout(const int32_t* idx, int64_t T, int k, int E, int R, int fixed_cap,
                          int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
                          int32_t* rank_offset, int32_t* pos, int32_t* row_src, void* workspace,
-                         uint32_t* status, hipStream_t stream) {
+                         uint32_t* status, hipStream_t stream, int peer_L) {
   if (fixed_cap >= 0)
-    return launch_layout_fx<true>(idx, T, k, E, R, fixed_cap, expert_count, expert_offset,
-                                  rank_count, rank_offset, pos, row_src, workspace, status,
-                                  stream);
-  return launch_layout_fx<false>(idx, T, k, E, R, 0, expert_count, expert_offset, rank_count,
-                                 rank_offset, pos, row_src, workspace, status, stream);
+    return launch_layout_fx<true>(idx, T, k, E, peer_L, R, fixed_cap, expert_count,
+                                  expert_offset, rank_count, rank_offset, pos, row_src, workspace,
+                                  status, stream);
+  return launch_layout_fx<false>(idx, T, k, E, peer_L, R, 0, expert_count, expert_offset,
+                                 rank_count, rank_offset, pos, row_src, workspace, status, stream);
 }
 
 }  // namespace moe

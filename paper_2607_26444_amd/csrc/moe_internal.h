@@ -60,11 +60,13 @@ constexpr int64_t kDispatchInFlight = 64ll << 20;
 constexpr int64_t kCombineInFlight = 16ll << 20;
 
 // fixed_cap < 0: packed layout; >= 0: fixed windows of fixed_cap rows.
+// peer_L > 0: topk_idx holds experts in [0, E * peer_L) and the layout is
+// over the E peers, one row per (token, peer) pair (first slot of the pair).
 hipError_t launch_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
                          int fixed_cap, int32_t* expert_count, int32_t* expert_offset,
                          int32_t* rank_count, int32_t* rank_offset, int32_t* pos,
                          int32_t* row_src, void* workspace, uint32_t* status,
-                         hipStream_t stream);
+                         hipStream_t stream, int peer_L = 0);
 
 struct DispatchArgs {
   const uint8_t* x;

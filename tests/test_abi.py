@@ -144,7 +144,7 @@ def test_dedup_argument_errors():
     L = moe.lib()
     n = moe.moe_layout_dedup_workspace_bytes(64, 8, 256, 64)
     n_slot = moe.moe_layout_workspace_bytes(64, 8, 256, 64)
-    assert n >= (moe.MOE_PLAN_PARTS + 1) * 4 + 64 * 8 * 4
+    assert n >= (moe.MOE_PLAN_PARTS + 1) * 4 + (2 * 64 + 1) * 4
     out = ctypes.c_size_t(0)
     assert L.moe_layout_dedup_workspace_bytes(16, 8, 256, 60, ctypes.byref(out)) == moe.MOE_EINVAL
     # layout
