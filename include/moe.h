@@ -31,7 +31,8 @@
  *  - Return codes (host side, checked before anything is enqueued; on error
  *    nothing is launched): MOE_OK, MOE_EINVAL (null pointer where one is
  *    required, T < 0, k < 1, k > MOE_MAX_K, k > E, E % R != 0,
- *    E > MOE_MAX_EXPERTS, T*k > INT32_MAX, H < 1, bad dtype), MOE_EALIGN (x
+ *    E > MOE_MAX_EXPERTS, T*k > INT32_MAX, H < 1, a row of more than
+ *    INT32_MAX bytes, bad dtype), MOE_EALIGN (x
  *    or y not 16-byte aligned, row bytes not a multiple of 16, fp8 H not a
  *    multiple of 128, x_scales not 4-byte aligned; region base addresses sit
  *    in device tables and their alignment is the caller's to keep),

@@ -62,6 +62,9 @@ bool waves_ok(int waves) {
          waves % moe::kWavesPerBlock == 0 && MOE_PLAN_PARTS % waves == 0;
 }
 
+// Kernels address within a row with 32-bit offsets: rows stay below 2 GiB.
+bool row_fits(int64_t row_bytes) { return row_bytes <= (int64_t)INT32_MAX; }
+
 int shape_ok(int64_t T, int k, int E, int R) {
   if (T < 0 || k < 1 || k > MOE_MAX_K || E < 1 || E > MOE_MAX_EXPERTS || R < 1 || k > E ||
       E % R != 0)
@@ -177,6 +180,7 @@ int dispatch_common(const void* x, const float* x_scales, int dtype, int64_t T, 
     return MOE_EINVAL;
   if (trace && trace_waves < 0) return MOE_EINVAL;
   const int64_t row_bytes = fp8 ? (int64_t)H : 2 * (int64_t)H;
+  if (!row_fits(row_bytes)) return MOE_EINVAL;
   if (row_bytes % 16 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
   if (!aligned(x, 16) || (fp8 && !aligned(x_scales, 4))) return MOE_EALIGN;
   const int scale_row = fp8 ? (H / MOE_FP8_BLOCK) * 4 : 0;
@@ -254,7 +258,7 @@ int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weig
                    uint64_t* trace, int trace_waves, int rows_hint, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
-  if (H < 1) return MOE_EINVAL;
+  if (H < 1 || !row_fits(2 * (int64_t)H)) return MOE_EINVAL;
   if (!expert_y || !recv_cap || !rank_offset || !workspace || !status) return MOE_EINVAL;
   if (T > 0 && ((!unit_weights && !topk_w) || !topk_idx || !pos || !y)) return MOE_EINVAL;
   if (policy != MOE_POLICY_BALANCED && policy != MOE_POLICY_DYNAMIC &&
@@ -318,7 +322,8 @@ int moe_expert_scale(const uint64_t* recv_x, const uint64_t* recv_scales, int sc
                      const int32_t* expert_offset, const int32_t* rank_offset,
                      const int32_t* recv_cap, const uint64_t* out_y, int64_t max_rows,
                      void* stream) {
-  if (H < 1 || E < 1 || E > MOE_MAX_EXPERTS || R < 1 || E % R != 0 || max_rows < 0)
+  if (H < 1 || !row_fits(2 * (int64_t)H) || E < 1 || E > MOE_MAX_EXPERTS || R < 1 ||
+      E % R != 0 || max_rows < 0)
     return MOE_EINVAL;
   if (dtype != MOE_DTYPE_BF16 && dtype != MOE_DTYPE_FP8_E4M3) return MOE_EINVAL;
   const bool fp8 = dtype == MOE_DTYPE_FP8_E4M3;
@@ -401,6 +406,7 @@ int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype,
   if (fp8 && (!dedup_scales || !recv_scales)) return MOE_EINVAL;
   if (T > 0 && (!topk_idx || !pos || !tok_pos)) return MOE_EINVAL;
   const int64_t row_bytes = fp8 ? (int64_t)H : 2 * (int64_t)H;
+  if (!row_fits(row_bytes)) return MOE_EINVAL;
   if (row_bytes % 16 != 0 || (fp8 && H % MOE_FP8_BLOCK != 0)) return MOE_EALIGN;
   const int scale_row = fp8 ? (H / MOE_FP8_BLOCK) * 4 : 0;
   const int pitch = (fp8 && scale_pitch == 0) ? scale_row : scale_pitch;
@@ -441,7 +447,7 @@ int moe_combine_local(const uint64_t* expert_y, const float* topk_w, int64_t T, 
                       size_t workspace_bytes, uint32_t* status, void* stream) {
   int rc = shape_ok(T, k, E, R);
   if (rc) return rc;
-  if (H < 1) return MOE_EINVAL;
+  if (H < 1 || !row_fits(2 * (int64_t)H)) return MOE_EINVAL;
   if (!expert_y || !recv_cap || !rank_offset || !tok_offset || !part_cap || !partial ||
       !workspace || !status)
     return MOE_EINVAL;

@@ -112,6 +112,8 @@ def test_dispatch_argument_errors():
     for w in (-4, 2, 6, 20, 12292, 24576):             # not a divisor of the plan / of 4
         assert L.moe_dispatch_ex(*_dispatch_args(waves=w)) == moe.MOE_EINVAL
     assert L.moe_dispatch_ex(*_dispatch_args(policy=2, rs=FAKE, waves=96)) == moe.MOE_EINVAL
+    # rows of 2 GiB or more: in-row offsets are 32-bit
+    assert L.moe_dispatch_ex(*_dispatch_args(H=2 ** 30)) == moe.MOE_EINVAL
 
 
 def test_combine_argument_errors():
@@ -130,6 +132,8 @@ def test_combine_argument_errors():
     bad = list(ok); bad[15] = moe.MOE_POLICY_ROWS      # pull splits are dispatch-only
     assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
     bad = list(ok); bad[16] = 100                      # does not divide the plan
+    assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
+    bad = list(ok); bad[3] = 2 ** 30                   # a 2 GiB output row
     assert L.moe_combine_ex(*bad) == moe.MOE_EINVAL
 
 
