@@ -38,6 +38,17 @@ def test_binding_covers_every_declared_symbol():
     assert sorted(moe.EXPORTS) == declared_functions()
 
 
+def test_binding_constants_match_the_header():
+    text = open(HEADER).read()
+    defines = dict(re.findall(r"^#define\s+(MOE_\w+)\s+\(?(-?\d+)u?\)?", text, flags=re.M))
+    for name in ("MOE_PLAN_PARTS", "MOE_POLICY_STATIC", "MOE_EINVAL", "MOE_STATUS_CAPACITY"):
+        assert name in defines, name
+    assert moe.moe_version() == int(defines.pop("MOE_VERSION"))
+    for name, value in defines.items():
+        assert hasattr(moe, name), name
+        assert getattr(moe, name) == int(value), name
+
+
 def test_version_and_strerror():
     assert moe.moe_version() == 4
     for code in (0, -1, -2, -3, -4, -99):
