@@ -441,6 +441,10 @@ def main(argv=None):
                     help="instead of the step benchmark: dispatch under each work split")
     ap.add_argument("--ll", type=float, default=None, metavar="F",
                     help="fixed-capacity layout with windows of F x the mean expert load")
+    ap.add_argument("--x-copies", type=int, default=0, metavar="N",
+                    help="hidden-state copies the timed steps cycle through (0: enough to "
+                         "fill 512 MiB, at most 16, so a step's x is not in the 256 MB "
+                         "Infinity Cache; 1: every step reads the same x)")
     ap.add_argument("--cold-reps", type=int, default=20,
                     help="repetitions of the cold-cache pass (0 skips it)")
     ap.add_argument("--dedup", action="store_true",
@@ -478,6 +482,15 @@ def main(argv=None):
     xs_d = torch.from_numpy(inp["x_scales"]).to(dev) if fp8 else None
     idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
     w_d = torch.from_numpy(inp["topk_w"]).to(dev)
+    # Each step reads its own copy of the hidden states (as each layer of a
+    # model has its own): cycling through copies that fill 512 MiB keeps a
+    # step from finding its x in the 256 MB Infinity Cache, where the
+    # previous step's read would otherwise leave it (everything else in the
+    # step is streamed non-temporally past the cache).
+    n_x = a.x_copies if a.x_copies > 0 else min(16, max(1, -(-(512 << 20) // x_d.numel())))
+    xs_all = [(x_d, xs_d)] + [(x_d.clone(), xs_d.clone() if fp8 else None)
+                              for _ in range(n_x - 1)]
+    cur = [0]
 
     if a.graph and a.ll is None:
         print("--graph needs --ll (the packed layout reads counts back to size regions)",
@@ -500,7 +513,8 @@ def main(argv=None):
     y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
 
     def dispatch():
-        moe.moe_dispatch(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
+        xc, xsc = xs_all[cur[0]]
+        moe.moe_dispatch(xc, xsc, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
                          regions.table, sregions.table if fp8 else None, regions.cap,
                          lay.workspace, lay.status, scale_pitch=spitch)
 
@@ -515,7 +529,8 @@ def main(argv=None):
                          regions.cap, eregions.table, sum(rows), scale_pitch=spitch)
     torch.cuda.synchronize()
 
-    for _ in range(a.warmup):
+    for i in range(a.warmup):
+        cur[0] = i % n_x
         lay.run(idx_d)
         dispatch()
         combine()
@@ -533,24 +548,31 @@ def main(argv=None):
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
     graph = None
     if a.graph:
-        # one graph per step; events stay outside it (recorded around replays)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            lay.run(idx_d)
-            dispatch()
-            combine()
+        # one graph per step and x copy; events stay outside it (recorded
+        # around replays)
+        graph = []
+        for i in range(n_x):
+            cur[0] = i
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                lay.run(idx_d)
+                dispatch()
+                combine()
+            graph.append(g)
         torch.cuda.synchronize()
         for _ in range(3):
-            graph.replay()
+            for g in graph:
+                g.replay()
         torch.cuda.synchronize()
         stream = torch.cuda.current_stream()
     print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(a.steps):
+        cur[0] = s % n_x
         ev[s][0].record(stream)
         if graph is not None:
-            graph.replay()
+            graph[cur[0]].replay()
             ev[s][1].record(stream)
             ev[s][2].record(stream)
         else:
@@ -605,7 +627,7 @@ def main(argv=None):
                    "payload": "fp8_e4m3" if fp8 else "bf16", "zipf_s": cfg["zipf_s"],
                    "force_frac": cfg["force_frac"], "parallelism": "1 GPU, R emulated ranks",
                    "layout": "packed" if capacity is None else f"fixed windows of {capacity}",
-                   "graph": bool(graph is not None)},
+                   "graph": bool(graph is not None), "x_copies": n_x},
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "tokens_per_s": round(T / (step_ms * 1e-3), 1),
         "layout_us": _num(l_us, 2),
