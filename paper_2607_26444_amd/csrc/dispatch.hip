@@ -57,8 +57,26 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     s_dst[wv][kWave + lane] = 0;
     if (SCALES) s_sdst[wv][kWave + lane] = 0;
   }
+  // Rows that fit in one pass (row bytes <= VPL KiB) are loaded one token
+  // ahead: the next token's row is requested before the current one is
+  // stored, so its loads complete while the stores drain instead of after
+  // them (loads and stores share one in-order completion counter).
+  const bool one_pass = rb <= (uint32_t)(VPL * kWaveBytes);
+  const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
+  u32x4 vn[VPL];
+  u32x4 svn = {0u, 0u, 0u, 0u};
+  int pre_t = -1;   // token whose row vn holds (-1: none)
+  auto load_row = [&](u32x4 (&v)[VPL], u32x4& sv, int t) {
+    const uint8_t* src = a.x + (int64_t)t * rb;
+#pragma unroll
+    for (int c = 0; c < VPL; ++c) {
+      const uint32_t off = c * kWaveBytes + l16;
+      if (FULL || off < rb) v[c] = ld16(src + off);
+    }
+    if (s16 && l16 < sb) sv = ld16(a.x_scales + (int64_t)t * sb + l16);
+  };
 
-  for_each_part<MODE>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
+  for_each_part<MODE, true>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1, int next) {
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t dst = 0, sdst = 0;
@@ -88,7 +106,32 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
       // Scale rows (pitch up to 1 KiB, sizes in 16-byte multiples) move with
       // the row: lane l carries bytes [16 l, 16 l + 16) of the pitched row,
       // scales first, zeros after.
-      const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
+      if (one_pass) {
+        u32x4 v[VPL];
+        u32x4 sv = {0u, 0u, 0u, 0u};
+        if (pre_t == t) {
+#pragma unroll
+          for (int c = 0; c < VPL; ++c) v[c] = vn[c];
+          sv = svn;
+        } else {
+          load_row(v, sv, t);
+        }
+        pre_t = t + 1 < t1 ? t + 1 : next;
+        if (pre_t >= 0) load_row(vn, svn, pre_t);
+        for (int j = 0; j < k; ++j) {
+          uint8_t* d = reinterpret_cast<uint8_t*>(readlane64(s_dst[wv][l0 + j], 0));
+          if (!d) continue;
+#pragma unroll
+          for (int c = 0; c < VPL; ++c) {
+            const uint32_t off = c * kWaveBytes + l16;
+            if (FULL || off < rb) st16_stream(d + off, v[c]);
+          }
+          if (s16) {
+            uint8_t* sd = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l0 + j], 0));
+            if (l16 < sp) st16_stream(sd + l16, sv);
+          }
+        }
+      } else {
       u32x4 sv = {0u, 0u, 0u, 0u};
       if (s16 && l16 < sb) sv = ld16(ssrc + l16);
       for (uint32_t seg = 0; seg < rb; seg += VPL * kWaveBytes) {
@@ -111,6 +154,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
             if (l16 < sp) st16_stream(sd + l16, sv);
           }
         }
+      }
       }
       if (SCALES && !s16) {
         // Other scale-row sizes: one float32 per lane per pass.

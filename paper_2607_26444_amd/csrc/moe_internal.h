@@ -200,7 +200,10 @@ __device__ __forceinline__ void finish_parts(uint32_t* tickets, int W, int lane)
 // handles under MODE.  Part boundaries are fetched up to 64 at a time, one
 // part per lane, so stepping to the next part (often an empty one when there
 // are fewer tokens than parts) costs no global-memory round trip each.
-template <int MODE, typename F>
+// PEEK: body(t0, t1, next) also gets the first token of the next non-empty
+// part this wavefront will take when that is already known (a later part of
+// the same fetched group), else -1, so the body can start loading it early.
+template <int MODE, bool PEEK = false, typename F>
 __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* tickets, int g,
                                               int W, int lane, F&& body) {
   // static share: parts g + i*W below S
@@ -208,6 +211,16 @@ __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* ti
                 : MODE == kPartsHybrid ? (MOE_PLAN_PARTS / 2) / W * W
                                        : (g < MOE_PLAN_PARTS ? g + 1 : g);
   const int m = MODE == kPartsClaimed ? (g < MOE_PLAN_PARTS ? 1 : 0) : (S - g + W - 1) / W;
+  auto call = [&](int b0, int b1, uint64_t nonempty, int i) {
+    const int t0 = __builtin_amdgcn_readlane(b0, i), t1 = __builtin_amdgcn_readlane(b1, i);
+    if constexpr (PEEK) {
+      const uint64_t later = nonempty & ~((2ull << i) - 1ull);   // lanes above i
+      const int next = later ? __builtin_amdgcn_readlane(b0, __builtin_ctzll(later)) : -1;
+      body(t0, t1, next);
+    } else {
+      body(t0, t1);
+    }
+  };
   for (int i0 = 0; i0 < m; i0 += kWave) {
     int b0 = 0, b1 = 0;
     if (i0 + lane < m) {
@@ -215,9 +228,9 @@ __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* ti
       b0 = (int)ld4(bound + part);
       b1 = (int)ld4(bound + part + 1);
     }
+    const uint64_t nonempty = PEEK ? __ballot(b0 < b1) : 0ull;
     const int n = m - i0 < kWave ? m - i0 : kWave;
-    for (int i = 0; i < n; ++i)
-      body(__builtin_amdgcn_readlane(b0, i), __builtin_amdgcn_readlane(b1, i));
+    for (int i = 0; i < n; ++i) call(b0, b1, nonempty, i);
   }
   if (MODE == kPartsStatic) return;
   // claimed share: parts from `first` on, G per ticket
@@ -233,9 +246,9 @@ __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* ti
       b0 = (int)ld4(bound + p0 + lane);
       b1 = (int)ld4(bound + p0 + lane + 1);
     }
+    const uint64_t nonempty = PEEK ? __ballot(b0 < b1) : 0ull;
     const int n = MOE_PLAN_PARTS - p0 < G ? MOE_PLAN_PARTS - p0 : G;
-    for (int i = 0; i < n; ++i)
-      body(__builtin_amdgcn_readlane(b0, i), __builtin_amdgcn_readlane(b1, i));
+    for (int i = 0; i < n; ++i) call(b0, b1, nonempty, i);
   }
 }
 
