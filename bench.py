@@ -188,6 +188,18 @@ def trace_stats(trace, khz):
                 busy_mean_us=round(float(busy.mean()), 2))
 
 
+def hidden_copies(x_d, xs_d, n):
+    """Copies of the hidden states (and fp8 scales) for the timed steps to
+    cycle through, each step reading its own as each layer of a model does.
+    n = 0: copies that fill 512 MiB (at most 16), so a step does not find
+    its x in the 256 MB Infinity Cache, where the previous read of the same
+    x would otherwise leave it (the rest of a step streams non-temporally
+    past the cache)."""
+    n = n if n > 0 else min(16, max(1, -(-(512 << 20) // x_d.numel())))
+    return [(x_d, xs_d)] + [(x_d.clone(), None if xs_d is None else xs_d.clone())
+                            for _ in range(n - 1)]
+
+
 def ablation(a):
     """Dispatch under the three work splits of moe_dispatch_ex on one
     workload: kernel time (HIP events) and the per-wavefront completion trace.
@@ -205,6 +217,8 @@ def ablation(a):
     stream = torch.cuda.current_stream()
     x_d = torch.from_numpy(np.ascontiguousarray(inp["x"]).view(np.uint8)).to(dev)
     xs_d = torch.from_numpy(inp["x_scales"]).to(dev) if fp8 else None
+    xs_all = hidden_copies(x_d, xs_d, a.x_copies)
+    n_calls = [0]
     idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
     lay = moe.Layout(T, k, E, R)
     lay.run(idx_d)
@@ -216,14 +230,17 @@ def ablation(a):
     sregions = moe.Regions(rows, spitch) if fp8 else None
     trace = torch.zeros(2 * moe.MOE_PLAN_PARTS, dtype=torch.int64, device=dev)
     khz = moe.moe_wall_clock_khz()
-    out = {"metric": "dispatch work-split ablation", "config": {"workload": cfg["name"]},
+    out = {"metric": "dispatch work-split ablation",
+           "config": {"workload": cfg["name"], "x_copies": len(xs_all)},
            "rank_rows_max_over_mean": round(max(rows) / (sum(rows) / len(rows)), 2),
            "wall_clock_khz": khz, "policies": {}}
     b = algorithmic_bytes(cfg)
 
     def time_dispatch(pol, waves=0):
         def run(tr=None):
-            moe.moe_dispatch_ex(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
+            xc, xsc = xs_all[n_calls[0] % len(xs_all)]
+            n_calls[0] += 1
+            moe.moe_dispatch_ex(xc, xsc, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
                                 lay.row_src, regions.table,
                                 sregions.table if fp8 else None, regions.cap, lay.workspace,
                                 lay.status, policy=pol, trace=tr, scale_pitch=spitch,
@@ -318,6 +335,8 @@ def dedup_bench(a):
     stream = torch.cuda.current_stream()
     x_d = torch.from_numpy(np.ascontiguousarray(inp["x"]).view(np.uint8)).to(dev)
     xs_d = torch.from_numpy(inp["x_scales"]).to(dev) if fp8 else None
+    xs_all = hidden_copies(x_d, xs_d, a.x_copies)
+    cur = [0]
     idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
     w_d = torch.from_numpy(inp["topk_w"]).to(dev)
     lay = moe.Layout(T, k, E, R)
@@ -343,7 +362,7 @@ def dedup_bench(a):
         "layout": lambda: lay.run(idx_d),
         "layout_dedup": lambda: dl.run(idx_d),
         "dispatch_dedup": lambda: moe.moe_dispatch_dedup(
-            x_d, xs_d, dtype, H, E, R, idx_d, dl.tok_pos, dl.tok_offset, dreg.table,
+            *xs_all[cur[0]], dtype, H, E, R, idx_d, dl.tok_pos, dl.tok_offset, dreg.table,
             dsreg.table if fp8 else None, dreg.cap, dl.workspace, status, scale_pitch=spitch),
         "expand": lambda: moe.moe_expand(
             dreg.table, dsreg.table if fp8 else None, dtype, H, E, R, idx_d, lay.pos,
@@ -356,7 +375,7 @@ def dedup_bench(a):
             preg.table, H, E, R, idx_d, dl.tok_pos, dl.tok_offset, preg.cap, y, dl.workspace,
             status),
         "dispatch": lambda: moe.moe_dispatch(
-            x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset, reg.table,
+            *xs_all[cur[0]], dtype, H, E, R, idx_d, lay.pos, lay.rank_offset, reg.table,
             sreg.table if fp8 else None, reg.cap, lay.workspace, status, scale_pitch=spitch),
         "combine": lambda: moe.moe_combine(
             ereg.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, ereg.cap, y,
@@ -368,13 +387,15 @@ def dedup_bench(a):
                          reg.cap, ereg.table, sum(rows), scale_pitch=spitch)
     torch.cuda.synchronize()
     names = list(ops)
-    for _ in range(a.warmup):
+    for i in range(a.warmup):
+        cur[0] = i % len(xs_all)
         for n in names:
             ops[n]()
     torch.cuda.synchronize()
     ev = {n: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(a.steps)] for n in names}
     for s_ in range(a.steps):
+        cur[0] = s_ % len(xs_all)
         for n in names:
             ev[n][s_][0].record(stream)
             ops[n]()
@@ -401,7 +422,7 @@ def dedup_bench(a):
     out = {
         "metric": "per-peer deduplicated dispatch/combine: per-kernel HBM GB/s",
         "config": {"workload": cfg["name"], "T": T, "H": H, "E": E, "R": R, "k": k,
-                   "payload": "fp8_e4m3" if fp8 else "bf16"},
+                   "payload": "fp8_e4m3" if fp8 else "bf16", "x_copies": len(xs_all)},
         "steps": a.steps, "warmup": a.warmup,
         "slots": n_slots, "pair_rows": n_pairs,
         "pair_row_fraction": round(n_pairs / max(1, n_slots), 4),
@@ -482,14 +503,8 @@ def main(argv=None):
     xs_d = torch.from_numpy(inp["x_scales"]).to(dev) if fp8 else None
     idx_d = torch.from_numpy(inp["topk_idx"]).to(dev)
     w_d = torch.from_numpy(inp["topk_w"]).to(dev)
-    # Each step reads its own copy of the hidden states (as each layer of a
-    # model has its own): cycling through copies that fill 512 MiB keeps a
-    # step from finding its x in the 256 MB Infinity Cache, where the
-    # previous step's read would otherwise leave it (everything else in the
-    # step is streamed non-temporally past the cache).
-    n_x = a.x_copies if a.x_copies > 0 else min(16, max(1, -(-(512 << 20) // x_d.numel())))
-    xs_all = [(x_d, xs_d)] + [(x_d.clone(), xs_d.clone() if fp8 else None)
-                              for _ in range(n_x - 1)]
+    xs_all = hidden_copies(x_d, xs_d, a.x_copies)
+    n_x = len(xs_all)
     cur = [0]
 
     if a.graph and a.ll is None:

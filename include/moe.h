@@ -204,11 +204,14 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
 
 /* Work-split policies of moe_dispatch_ex / moe_combine_ex (all give
  * bit-identical regions and identical y). */
-#define MOE_POLICY_BALANCED 0 /* byte-balanced parts, the library's choice: dispatch
-                               * assigns the first half of the parts statically and
-                               * hands the rest out at run time (all statically when
-                               * a wavefront would own fewer than 8 parts); combine
-                               * assigns all statically (moe_dispatch, moe_combine) */
+#define MOE_POLICY_BALANCED 0 /* byte-balanced parts, the library's choice: when a
+                               * part carries 128 KiB or more on average, every part
+                               * after each wavefront's first is handed out at run
+                               * time (dispatch and combine); smaller parts: dispatch
+                               * assigns the first half statically and hands the rest
+                               * out at run time (all statically when a wavefront
+                               * would own fewer than 8 parts), combine assigns all
+                               * statically (moe_dispatch, moe_combine) */
 #define MOE_POLICY_ROWS 1     /* pull: the N routed rows split evenly over wavefronts */
 #define MOE_POLICY_BY_RANK 2  /* pull: a fixed group of W/R wavefronts per rank */
 #define MOE_POLICY_DYNAMIC 3  /* push; every part after the first handed out at run time */

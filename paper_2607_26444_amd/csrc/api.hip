@@ -192,6 +192,7 @@ int dispatch_common(const void* x, const float* x_scales, int dtype, int64_t T, 
   moe::DispatchArgs a;
   a.x = static_cast<const uint8_t*>(x);
   a.x_scales = fp8 ? reinterpret_cast<const uint8_t*>(x_scales) : nullptr;
+  a.tokens = T;
   a.row_bytes = row_bytes;
   a.scale_row_bytes = scale_row;
   a.scale_pitch = fp8 ? pitch : 0;
@@ -272,6 +273,7 @@ int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weig
   moe::CombineArgs a;
   a.expert_y = expert_y;
   a.topk_w = unit_weights ? nullptr : topk_w;
+  a.tokens = T;
   a.row_bytes = 2 * (int64_t)H;
   a.k = k;
   a.L = E / R;

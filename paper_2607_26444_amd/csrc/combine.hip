@@ -1,7 +1,9 @@
 // Combine: y[t] = bf16( sum_j w[t,j] * Y(row of slot j) ).
 //
 // Token-centric gather-reduce with the same byte-balanced partition as
-// dispatch (wavefront g of W takes parts g, g + W, ... of the plan).  Slot metadata for a batch
+// dispatch (wavefront g of W takes parts g, g + W, ... of the plan; under the
+// default split every later part is handed out at run time instead when
+// parts are large, kClaimAllPartBytes).  Slot metadata for a batch
 // of 64/k tokens is resolved once, one slot per lane, and parked in LDS; for
 // each token the wavefront reads its k source rows and weights back at
 // uniform LDS addresses (waiting only on the LDS counter, never on pending
@@ -273,8 +275,10 @@ hipError_t launch_dyn(const CombineArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_combine(const CombineArgs& a, int policy, hipStream_t stream) {
-  return policy == MOE_POLICY_DYNAMIC ? launch_dyn<true>(a, stream)
-                                      : launch_dyn<false>(a, stream);
+  const int64_t rows = a.rows_hint > 0 ? a.rows_hint : a.k;
+  const bool claim = policy == MOE_POLICY_DYNAMIC ||
+                     (policy == MOE_POLICY_BALANCED && claim_all_parts(a.tokens, a.row_bytes, rows));
+  return claim ? launch_dyn<true>(a, stream) : launch_dyn<false>(a, stream);
 }
 
 }  // namespace moe

@@ -10,7 +10,11 @@
 // wavefronts work on neighbouring parts, so x is read and each expert window
 // is written as one advancing front instead of W scattered streams (on
 // MI355X that measured ~5% faster for dispatch and ~7% for combine than
-// giving each wavefront one contiguous run of parts).
+// giving each wavefront one contiguous run of parts).  Equal bytes are not
+// equal time on a shared memory system, so under the default split parts
+// are also handed out at run time from a workspace counter, in plan order
+// (the front is kept): every part after each wavefront's first when parts
+// are large (kClaimAllPartBytes), the second half of the parts otherwise.
 //
 // Push direction: a wavefront reads its token's row from x once into
 // registers (16 bytes per lane per 1 KiB segment, so a 14 KiB row is 14
@@ -314,7 +318,10 @@ hipError_t launch_vpl(DispatchArgs a, int policy, hipStream_t stream) {
   if (policy == MOE_POLICY_BY_RANK)
     return full ? launch_pull<VPL, true, SCALES, MOE_POLICY_BY_RANK>(a, stream)
                 : launch_pull<VPL, false, SCALES, MOE_POLICY_BY_RANK>(a, stream);
-  if (policy == MOE_POLICY_DYNAMIC) return launch_push<VPL, SCALES, kPartsClaimed>(a, stream);
+  const int64_t rows = a.rows_hint > 0 ? a.rows_hint : a.k;
+  if (policy == MOE_POLICY_DYNAMIC ||
+      (policy == MOE_POLICY_BALANCED && claim_all_parts(a.tokens, a.row_bytes, rows)))
+    return launch_push<VPL, SCALES, kPartsClaimed>(a, stream);
   return launch_push<VPL, SCALES, kPartsHybrid>(a, stream, policy == MOE_POLICY_STATIC);
 }
 

@@ -59,6 +59,20 @@ int copy_waves(const void* kernel, int64_t per_wave, int64_t target, int min_wav
 constexpr int64_t kDispatchInFlight = 64ll << 20;
 constexpr int64_t kCombineInFlight = 16ll << 20;
 
+// The default split (MOE_POLICY_BALANCED) hands every part out at run time
+// when a part carries at least this many algorithmic bytes on average
+// (tokens * row bytes * (1 + rows per token) / MOE_PLAN_PARTS).  Measured on
+// MI355X with a fresh x per step: claiming every part made dispatch 4-6% and
+// combine 2-4% faster at 168-192 KiB per part (prefill, large, fp8
+// combine), 1% slower at 84 KiB (fp8 dispatch) and 43-78% slower at 42 KiB
+// (decode), where one claim serves a third of a token and the claims
+// serialize on the counter.
+constexpr int64_t kClaimAllPartBytes = 128ll << 10;
+
+__host__ __forceinline__ bool claim_all_parts(int64_t tokens, int64_t row_bytes, int64_t rows) {
+  return tokens * row_bytes * (1 + rows) / MOE_PLAN_PARTS >= kClaimAllPartBytes;
+}
+
 // fixed_cap < 0: packed layout; >= 0: fixed windows of fixed_cap rows.
 // peer_L > 0: topk_idx holds experts in [0, E * peer_L) and the layout is
 // over the E peers, one row per (token, peer) pair (first slot of the pair).
@@ -71,6 +85,7 @@ hipError_t launch_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R
 struct DispatchArgs {
   const uint8_t* x;
   const uint8_t* x_scales;     // nullptr for bf16 payloads
+  int64_t tokens;              // T
   int64_t row_bytes;           // 2H (bf16) or H (fp8)
   int32_t scale_row_bytes;     // (H/128)*4 or 0
   int32_t scale_pitch;         // bytes between scale rows of a region (>= scale_row_bytes)
@@ -98,6 +113,7 @@ hipError_t launch_dispatch(const DispatchArgs& a, int policy, hipStream_t stream
 struct CombineArgs {
   const uint64_t* expert_y;
   const float* topk_w;         // nullptr: every weight is 1
+  int64_t tokens;              // T
   int64_t row_bytes;           // 2H
   int32_t k;
   int32_t L;
