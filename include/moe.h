@@ -188,9 +188,10 @@ int moe_layout_fixed(const int32_t* topk_idx, int64_t T, int k, int E, int R, in
  *           wavefronts write partially; packed 224-byte rows cost ~30 us more
  *           per 131k rows on MI355X.
  * recv_cap  [R] int32 capacity of each region in rows.
- * topk_idx, pos, rank_offset, workspace: as produced by moe_layout.  The
- *           second half of the plan's parts is handed out at run time from
- *           a counter in the workspace (MOE_POLICY_BALANCED of
+ * topk_idx, pos, rank_offset, workspace: as produced by moe_layout.  Parts
+ *           of the plan are handed out at run time from a counter in the
+ *           workspace (all but each wavefront's first when parts carry 128
+ *           KiB or more, else the second half; MOE_POLICY_BALANCED of
  *           moe_dispatch_ex): two dispatch calls that share a workspace must
  *           not run at the same time on different streams.
  * Bytes of a region beyond the rows dispatch writes are left untouched.
@@ -225,14 +226,16 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
  * the same pull work evenly, MOE_POLICY_BALANCED is the product path).
  *
  * policy       one of MOE_POLICY_*; anything else is MOE_EINVAL.  Parts
- *              handed out at run time (MOE_POLICY_DYNAMIC, and the second half
- *              under MOE_POLICY_BALANCED) are claimed in plan order from a
- *              counter in the workspace (moe_layout zeroes it; the last
- *              wavefront of a launch resets it), so faster wavefronts take
- *              more parts.  Dispatch calls that share a workspace must
- *              therefore not run concurrently under these policies (nor
- *              combine calls under MOE_POLICY_DYNAMIC); calls one after
- *              another on a stream, or replayed in a graph, are fine.
+ *              handed out at run time (MOE_POLICY_DYNAMIC, and under
+ *              MOE_POLICY_BALANCED all of them for large parts or the second
+ *              half of dispatch's for small ones) are claimed in plan order
+ *              from a counter in the workspace (moe_layout zeroes it; the
+ *              last wavefront of a launch resets it), so faster wavefronts
+ *              take more parts.  Dispatch calls that share a workspace must
+ *              therefore not run concurrently under these policies, nor
+ *              combine calls (dispatch and combine use separate counters);
+ *              calls one after another on a stream, or replayed in a graph,
+ *              are fine.
  * waves        wavefronts to launch: 0 lets the library choose (the product
  *              choice; the push policies use the count of moe_dispatch, the
  *              pull policies as many as the device holds at once); otherwise
@@ -270,6 +273,11 @@ int moe_dispatch_ex(const void* x, const float* x_scales, int dtype, int64_t T, 
  * expert_y  [R] uint64 bf16 region bases (device table), 16-byte aligned.
  * topk_w    [T,k] float32.
  * y         [T,H] bf16 output, 16-byte aligned, 2H a multiple of 16.
+ * workspace as produced by moe_layout.  When parts carry 128 KiB or more,
+ *           all but each wavefront's first are handed out at run time from
+ *           a counter in the workspace (separate from dispatch's): two
+ *           combine calls that share a workspace must not run at the same
+ *           time on different streams.
  */
 int moe_combine(const uint64_t* expert_y, const float* topk_w, int64_t T, int H, int k,
                 int E, int R, const int32_t* topk_idx, const int32_t* pos,
