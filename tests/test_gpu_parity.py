@@ -364,7 +364,10 @@ def test_full_size_workloads(name):
     inp = wl.make_inputs(cfg)
     T, H, E, R, k = cfg["T"], cfg["H"], cfg["E"], cfg["R"], cfg["k"]
     h.log(f"[full] {cfg['name']}")
-    run = h.GpuRun(cfg, inp, spare_rows=1)
+    # two dispatch + combine calls on one layout: at these sizes the default
+    # split claims parts at run time, so the second call relies on the first
+    # one's counter reset
+    run = h.GpuRun(cfg, inp, spare_rows=1, repeat=2)
     lay = oracle.layout(inp["topk_idx"], E, R)
     for key in ("expert_count", "expert_offset", "rank_count", "rank_offset", "pos",
                 "row_src"):
