@@ -77,3 +77,35 @@ def test_random_shape_dedup_matches_oracle(seed):
     inp = wl.make_inputs(cfg)
     idx = wl.mask_slots(inp["topk_idx"], s["mask"], seed=seed) if s["mask"] else None
     _dedup_parity(cfg, inp, idx=idx)
+
+
+N_LARGE_CASES = 4
+
+
+def _large_shape(seed):
+    """A random batch large enough that the default split hands every part
+    out at run time (a plan part carries at least 128 KiB on average)."""
+    rng = np.random.default_rng(3000 + seed)
+    R = int(rng.choice([16, 32, 64]))
+    E = R * int(rng.choice([2, 4]))
+    k = 8 if seed % 2 == 0 else 6
+    fp8 = seed == 2   # fp8 rows: combine claims every part, dispatch's parts are smaller
+    H = 128 * int(rng.integers(40, 65)) if fp8 else 8 * int(rng.integers(640, 1025))
+    row_b = H if fp8 else 2 * H
+    T = int(rng.integers(12000, 20001))
+    while T * 2 * H * (1 + k) // 12288 < (128 << 10):   # combine's part bytes
+        T += 2048
+    return dict(T=T, H=H, E=E, R=R, k=k, fp8=fp8, row_b=row_b,
+                mask=float(rng.choice([0.0, 0.05])), zipf=float(rng.choice([0.0, 1.2])))
+
+
+@pytest.mark.parametrize("seed", range(N_LARGE_CASES))
+def test_random_large_batch_matches_oracle(seed):
+    from test_gpu_parity import _full_parity
+    s = _large_shape(seed)
+    cfg = wl.custom(s["T"], s["H"], s["E"], s["R"], s["k"],
+                    payload=wl.FP8_E4M3 if s["fp8"] else wl.BF16, zipf_s=s["zipf"],
+                    seed=7000 + seed)
+    inp = wl.make_inputs(cfg)
+    idx = wl.mask_slots(inp["topk_idx"], s["mask"], seed=seed) if s["mask"] else None
+    _full_parity(cfg, inp, idx=idx, repeat=2, spare_rows=1)
