@@ -147,3 +147,12 @@ def test_dedup_full_size(name):
     n_pairs = int(ref["dedup"]["tok_offset"][-1])
     _h().log(f"[dedup] {name}: {n_pairs} pair rows for {cfg['T'] * cfg['k']} slots "
              f"({n_pairs / (cfg['T'] * cfg['k']):.3f})")
+
+
+def test_dedup_large_batch_claims_every_part():
+    """24576 tokens of 14 KiB: the pair-row calls' parts carry ~140 KiB, so
+    their default split hands every part out at run time."""
+    cfg = wl.custom(24576, 7168, 256, 64, 8, zipf_s=1.2, seed=24576)
+    T, H, k = cfg["T"], cfg["H"], cfg["k"]
+    assert T * 2 * H * (1 + (k + 1) // 2) // moe.MOE_PLAN_PARTS >= 128 << 10
+    _dedup_parity(cfg)
