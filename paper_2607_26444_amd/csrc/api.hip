@@ -424,6 +424,7 @@ int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype,
   a.recv_x = recv_x;
   a.recv_scales = fp8 ? recv_scales : nullptr;
   a.recv_cap = recv_cap;
+  a.tokens = T;
   a.row_bytes = row_bytes;
   a.scale_row_bytes = scale_row;
   a.scale_pitch = fp8 ? pitch : 0;

@@ -27,6 +27,7 @@ struct ExpandArgs {
   const uint64_t* recv_x;        // [R] expert-ordered region bases
   const uint64_t* recv_scales;
   const int32_t* recv_cap;
+  int64_t tokens;                // T
   int64_t row_bytes;
   int32_t scale_row_bytes;
   int32_t scale_pitch;
