@@ -20,7 +20,13 @@
 //
 // Unused and capacity-dropped slots are redirected to a routed row of the
 // same token, their data is zeroed bitwise and their weight is 0 (a plain
-// multiply by 0 would turn an Inf in that row into NaN).
+// multiply by 0 would turn an Inf in that row into NaN).  When the caller
+// expects many unused slots (the source-side sum of the per-peer path, where
+// a token's later slots on a peer carry no row), each slot is read through a
+// buffer resource instead: an unused slot's resource has an empty range, so
+// its loads return +0 without a memory access and need no mask.  That
+// measured 8% faster for that sum at Zipf-skewed prefill; with every slot
+// routed the redirect measured ~1% faster at decode and is kept there.
 
 #include "moe_internal.h"
 
@@ -43,6 +49,20 @@ __device__ __forceinline__ void gather(u32x4 (&v)[KW], const uint8_t* const (&sr
                                        uint32_t off) {
 #pragma unroll
   for (int j = 0; j < KW; ++j) v[j] = ld16_stream(src[j] + off);
+}
+
+// Buffer resources (base, range in bytes): a load at an offset outside the
+// range returns zeros and reads nothing.  Word 3 selects 32-bit untyped data
+// on gfx9-family GPUs; cache policy 2 is the non-temporal hint.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kLoadNonTemporal = 2;
+
+template <int KW>
+__device__ __forceinline__ void gather(u32x4 (&v)[KW], const Rsrc (&src)[KW], uint32_t off) {
+#pragma unroll
+  for (int j = 0; j < KW; ++j)
+    v[j] = __builtin_amdgcn_raw_buffer_load_b128(src[j], off, 0, kLoadNonTemporal);
 }
 
 // Weighted sum of one 1 KiB segment.  MASKED: unused slots read a routed
@@ -75,8 +95,8 @@ __device__ __forceinline__ u32x4 reduce(const u32x4 (&v)[KW], const float (&wt)[
 // ragged tail.  The gathers of the next segment are issued before the
 // current one is reduced and stored, so waiting for them never waits for a
 // store (vector memory operations complete in issue order on this counter).
-template <int KW, bool MASKED>
-__device__ __forceinline__ void combine_row(uint8_t* dst, const uint8_t* const (&src)[KW],
+template <int KW, bool MASKED, typename S>
+__device__ __forceinline__ void combine_row(uint8_t* dst, const S (&src)[KW],
                                             const float (&wt)[KW],
                                             const uint32_t (&keep)[KW], uint32_t rb,
                                             uint32_t l16) {
@@ -116,10 +136,11 @@ __device__ __forceinline__ void store_row(uint8_t* dst, const u32x4 (&yr)[NSEG],
 // One token's output row of at most NSEG KiB, reduced into registers
 // (ceil(rb / 1 KiB) segments, the last one partial when rb is not a
 // multiple of 1 KiB) with the gathers two segments ahead as in combine_row,
-// then stored as one burst.  Always masked: the unrolled row is large, and
-// the mask is four ANDs per slot and segment (all ones for routed slots).
-template <int KW, int NSEG>
-__device__ __forceinline__ void combine_row_burst(uint8_t* dst, const uint8_t* const (&src)[KW],
+// then stored as one burst.  Masked whenever the slots are addressed by
+// pointer: the unrolled row is large, and the mask is four ANDs per slot and
+// segment (all ones for routed slots).
+template <int KW, int NSEG, bool MASKED, typename S>
+__device__ __forceinline__ void combine_row_burst(uint8_t* dst, const S (&src)[KW],
                                                   const float (&wt)[KW],
                                                   const uint32_t (&keep)[KW], uint32_t rb,
                                                   uint32_t l16) {
@@ -131,15 +152,16 @@ __device__ __forceinline__ void combine_row_burst(uint8_t* dst, const uint8_t* c
     if ((uint32_t)s < ns) {
       const uint32_t on = l16 + (uint32_t)(s + 1) * kWaveBytes;
       if (on < rb) gather<KW>(v[(s + 1) & 1], src, on);
-      yr[s] = reduce<KW, true>(v[s & 1], wt, keep);
+      yr[s] = reduce<KW, MASKED>(v[s & 1], wt, keep);
     }
   }
   store_row<NSEG>(dst, yr, rb, l16);
 }
 
 // KW: slots resolved per token (>= k).  NSEG > 0: rows of at most NSEG KiB,
-// each held in registers and stored as one burst (combine_row_burst).
-template <int KW, bool DYN, int NSEG>
+// each held in registers and stored as one burst (combine_row_burst).  BUF:
+// slots read through buffer resources, unused ones with an empty range.
+template <int KW, bool DYN, int NSEG, bool BUF>
 __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
   // Per-slot source row and weight of the current batch, one entry per lane
   // of each wavefront (0 = slot not combined), padded with zeros so a token
@@ -208,7 +230,8 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
       }
       uint8_t* dst = reinterpret_cast<uint8_t*>(a.y) + (int64_t)t * rb;
       if (!first) {  // no routed slot: y = +0
-        for (uint32_t off = l16; off < rb; off += kWaveBytes) st16_stream(dst + off, u32x4{0u, 0u, 0u, 0u});
+        for (uint32_t off = l16; off < rb; off += kWaveBytes)
+          st16_stream(dst + off, u32x4{0u, 0u, 0u, 0u});
         continue;
       }
       if (!all) {
@@ -216,8 +239,19 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
         for (int j = 0; j < KW; ++j)
           if (!keep[j]) src[j] = reinterpret_cast<const uint8_t*>(first);
       }
-      if constexpr (NSEG > 0) {
-        combine_row_burst<KW, NSEG>(dst, src, wt, keep, rb, l16);
+      if constexpr (BUF) {
+        Rsrc rs[KW];
+#pragma unroll
+        for (int j = 0; j < KW; ++j)
+          rs[j] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(src[j]), (short)0,
+                                                    keep[j] ? (int)rb : 0, kRsrcWord3);
+        if constexpr (NSEG > 0) {
+          combine_row_burst<KW, NSEG, false>(dst, rs, wt, keep, rb, l16);
+        } else {
+          combine_row<KW, false>(dst, rs, wt, keep, rb, l16);
+        }
+      } else if constexpr (NSEG > 0) {
+        combine_row_burst<KW, NSEG, true>(dst, src, wt, keep, rb, l16);
       } else if (all) {
         combine_row<KW, false>(dst, src, wt, keep, rb, l16);
       } else {
@@ -232,17 +266,17 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
   trace_wave(a.trace, a.trace_waves, g, t_start, lane);
 }
 
-template <int KW, bool DYN, int NSEG>
+template <int KW, bool DYN, int NSEG, bool BUF>
 hipError_t launch_kw(CombineArgs a, int64_t in_flight, hipStream_t stream) {
-  const void* fn = reinterpret_cast<const void*>(&combine_kernel<KW, DYN, NSEG>);
+  const void* fn = reinterpret_cast<const void*>(&combine_kernel<KW, DYN, NSEG, BUF>);
   // KW gathers of 1 KiB for each of the two segments in flight (of which
   // rows_hint read routed rows when the caller expects masked slots)
   const int64_t rows = a.rows_hint > 0 ? a.rows_hint : KW;
   const int waves = a.launch_waves > 0
                         ? a.launch_waves
                         : copy_waves(fn, 2 * rows * kWaveBytes, in_flight, 512);
-  hipLaunchKernelGGL((combine_kernel<KW, DYN, NSEG>), dim3(waves / kWavesPerBlock), dim3(kBlock),
-                     0, stream, a);
+  hipLaunchKernelGGL((combine_kernel<KW, DYN, NSEG, BUF>), dim3(waves / kWavesPerBlock),
+                     dim3(kBlock), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -253,12 +287,22 @@ hipError_t launch_kw(CombineArgs a, int64_t in_flight, hipStream_t stream) {
 // registers) store each segment as it is reduced.
 constexpr int kBurstSegs = 16;
 
-template <int KW, bool DYN>
-hipError_t launch_rows(const CombineArgs& a, int64_t in_flight, hipStream_t stream) {
+// Buffer-resource slots (BUF) when the caller expects unused slots
+// (rows_hint > 0) and the KW resources fit the scalar registers (KW <= 8).
+template <int KW, bool DYN, bool BUF>
+hipError_t launch_burst(const CombineArgs& a, int64_t in_flight, hipStream_t stream) {
   if (KW <= 8 && a.row_bytes >= 8ll * kWaveBytes &&
       a.row_bytes <= (int64_t)kBurstSegs * kWaveBytes)
-    return launch_kw<KW, DYN, (KW <= 8 ? kBurstSegs : 0)>(a, in_flight, stream);
-  return launch_kw<KW, DYN, 0>(a, in_flight, stream);
+    return launch_kw<KW, DYN, (KW <= 8 ? kBurstSegs : 0), BUF>(a, in_flight, stream);
+  return launch_kw<KW, DYN, 0, BUF>(a, in_flight, stream);
+}
+
+template <int KW, bool DYN>
+hipError_t launch_rows(const CombineArgs& a, int64_t in_flight, hipStream_t stream) {
+  if constexpr (KW <= 8) {
+    if (a.rows_hint > 0) return launch_burst<KW, DYN, true>(a, in_flight, stream);
+  }
+  return launch_burst<KW, DYN, false>(a, in_flight, stream);
 }
 
 template <bool DYN>
