@@ -319,8 +319,9 @@ hipError_t launch_vpl(DispatchArgs a, int policy, hipStream_t stream) {
     return full ? launch_pull<VPL, true, SCALES, MOE_POLICY_BY_RANK>(a, stream)
                 : launch_pull<VPL, false, SCALES, MOE_POLICY_BY_RANK>(a, stream);
   const int64_t rows = a.rows_hint > 0 ? a.rows_hint : a.k;
+  const int64_t min_part = a.rows_hint > 0 ? kClaimAllPairPartBytes : kClaimAllPartBytes;
   if (policy == MOE_POLICY_DYNAMIC ||
-      (policy == MOE_POLICY_BALANCED && claim_all_parts(a.tokens, a.row_bytes, rows)))
+      (policy == MOE_POLICY_BALANCED && claim_all_parts(a.tokens, a.row_bytes, rows, min_part)))
     return launch_push<VPL, SCALES, kPartsClaimed>(a, stream);
   return launch_push<VPL, SCALES, kPartsHybrid>(a, stream, policy == MOE_POLICY_STATIC);
 }
