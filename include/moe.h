@@ -79,10 +79,12 @@ extern "C" {
 #define MOE_MAX_EXPERTS 1024
 #define MOE_FP8_BLOCK 128
 
-/* Number of parts of the byte-balanced partition plan.  moe_dispatch and
- * moe_combine launch W wavefronts, W a power of two (512 to 4096, sized
- * from the bytes each wavefront keeps in flight) that divides P, and
- * wavefront g takes parts g, g+W, g+2W, ... (P/W parts of equal byte cost).
+/* Number of parts P of the byte-balanced partition plan (parts of equal byte
+ * cost).  moe_dispatch and moe_combine launch W wavefronts, W a power of
+ * two that divides P (dispatch 256 to 4096, combine 512 to 4096, sized from
+ * the bytes each wavefront keeps in flight).  Wavefront g starts at part g;
+ * later parts are either strided statically (g+W, g+2W, ...) or handed out
+ * at run time in plan order, as MOE_POLICY_BALANCED describes.
  * 12288 = 3 * 2^12 also divides evenly over 256 compute units at 4, 8, 12,
  * 16, 24 or 48 wavefronts each. */
 #define MOE_PLAN_PARTS 12288
