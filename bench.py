@@ -629,7 +629,11 @@ def main(argv=None):
                   f"--ll {need:.2f} or more", file=sys.stderr)
         return 1
 
-    ev = [[Event() for _ in range(4)] for _ in range(a.steps)]
+    # One event per phase boundary: the event that closes a step's combine
+    # also opens the next step's layout, so a step records three events (one
+    # around a graph replay).
+    per = 1 if a.graph else 3
+    ev = [Event() for _ in range(per * a.steps + 1)]
     graph = None
     if a.graph:
         # one graph per step and x copy; events stay outside it (recorded
@@ -652,20 +656,20 @@ def main(argv=None):
     print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev[0].record(stream)
     for s in range(a.steps):
         cur[0] = s % n_x
-        ev[s][0].record(stream)
+        e = ev[per * s:per * s + per + 1]
         if graph is not None:
             graph[cur[0]].replay()
-            ev[s][1].record(stream)
-            ev[s][2].record(stream)
+            e[1].record(stream)
         else:
             lay.run(idx_d)
-            ev[s][1].record(stream)
+            e[1].record(stream)
             dispatch()
-            ev[s][2].record(stream)
+            e[2].record(stream)
             combine()
-        ev[s][3].record(stream)
+            e[3].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     status = int(lay.status.item())
@@ -673,9 +677,13 @@ def main(argv=None):
         print(f"[bench] status word {status} after timing", file=sys.stderr)
         return 1
 
-    lay_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
-    dis_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
-    com_ms = np.array([e[2].elapsed_time(e[3]) for e in ev])
+    # (with a graph, lay_ms holds the whole replay)
+    lay_ms = np.array([ev[per * s].elapsed_time(ev[per * s + 1]) for s in range(a.steps)])
+    if graph is not None:
+        dis_ms = com_ms = np.full(a.steps, float("nan"))
+    else:
+        dis_ms = np.array([ev[3 * s + 1].elapsed_time(ev[3 * s + 2]) for s in range(a.steps)])
+        com_ms = np.array([ev[3 * s + 2].elapsed_time(ev[3 * s + 3]) for s in range(a.steps)])
     step_ms = wall * 1e3 / a.steps
     b = algorithmic_bytes(cfg)
     dc_bytes = b["dispatch"] + b["combine"]
@@ -683,7 +691,7 @@ def main(argv=None):
     d_us, c_us, l_us = dis_ms.mean() * 1e3, com_ms.mean() * 1e3, lay_ms.mean() * 1e3
     if graph is not None:
         # a replayed graph has no per-kernel events: whole-step figures only
-        # (the replay is timed between the step's first two events)
+        # (lay_ms times each replay)
         dom, dom_bytes, dom_us = "layout+dispatch+combine (graph)", dc_bytes, l_us
         d_us = c_us = l_us = float("nan")
         traffic = None
