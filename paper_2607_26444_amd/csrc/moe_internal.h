@@ -53,9 +53,9 @@ int resident_waves(const void* kernel, size_t lds_bytes);
 // one front.  On MI355X, whole workgroups spread evenly over the compute
 // units and a front of about 64 MiB of dispatch stores (16 MiB of combine
 // gathers, twice that for decode-sized batches whose parts are small) in
-// flight measured fastest over a range of preceding work; a 32 MiB dispatch
-// front is ~7% faster when dispatch follows combine but twice as slow after
-// a large ordinary-store kernel.
+// flight measured fastest over a range of preceding work; in a whole
+// layout -> dispatch -> combine step a 32 MiB dispatch front (half the
+// wavefronts) is 44-63% slower and a 128 MiB one ~4% slower.
 int copy_waves(const void* kernel, int64_t per_wave, int64_t target, int min_waves);
 constexpr int64_t kDispatchInFlight = 64ll << 20;
 constexpr int64_t kCombineInFlight = 16ll << 20;
