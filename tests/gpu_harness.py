@@ -82,12 +82,21 @@ class GpuRun:
         self.dtrace = torch.zeros(2 * moe.MOE_PLAN_PARTS, dtype=torch.int64,
                                   device="cuda") if trace else None
         self.ctrace = torch.zeros_like(self.dtrace) if trace else None
-        for _ in range(repeat):   # repeats reuse one layout (and its work tickets)
+        # Repeats reuse one layout and so its work tickets: before every
+        # repeat the outputs go back to the sentinel, so a call that skipped
+        # parts (a ticket counter left non-zero by the call before it) would
+        # leave sentinel bytes behind; after every call all tickets are zero.
+        for i in range(repeat):
+            if i > 0:
+                self.regions.buf.fill_(SENTINEL)
+                if fp8:
+                    self.sregions.buf.fill_(SENTINEL)
             moe.moe_dispatch_ex(x_d, xs_d, dtype, H, E, R, idx_d, lay.pos, lay.rank_offset,
                                 lay.row_src, self.regions.table,
                                 self.sregions.table if fp8 else None, cap_d, lay.workspace,
                                 lay.status, policy=policy, trace=self.dtrace,
                                 scale_pitch=self.scale_pitch, waves=waves)
+            check_tickets_zero(lay.workspace, f"dispatch call {i}")
 
         y = torch.empty((max(1, T), H), dtype=torch.int16, device="cuda")
         y.fill_(0x5A5A)
@@ -104,10 +113,13 @@ class GpuRun:
                                  max(1, T * k if capacity is None else E * capacity),
                                  scale_pitch=self.scale_pitch)
             ey_table = self.eregions.table
-        for _ in range(repeat):
+        for i in range(repeat):
+            if i > 0:
+                y.fill_(0x5A5A)
             moe.moe_combine_ex(ey_table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, cap_d,
                                y, lay.workspace, lay.status, policy=combine_policy,
                                trace=self.ctrace, waves=waves)
+            check_tickets_zero(lay.workspace, f"combine call {i}")
         torch.cuda.synchronize()
 
         nrows = T * k if capacity is None else E * capacity
@@ -125,6 +137,23 @@ class GpuRun:
 
     def region_bytes(self, regions):
         return regions.buf.cpu().numpy(), regions.offsets
+
+
+# The eight uint32 work tickets ({next part, wavefronts done} of dispatch,
+# combine and expand, then two spare) sit right after the plan, which is
+# bound[MOE_PLAN_PARTS + 1] padded to 256 bytes (the library's internal
+# workspace layout).
+TICKET_OFFSET = ((moe.MOE_PLAN_PARTS + 1) * 4 + 255) // 256 * 256
+
+
+def tickets(workspace) -> np.ndarray:
+    torch.cuda.synchronize()
+    return workspace[TICKET_OFFSET: TICKET_OFFSET + 32].view(torch.int32).cpu().numpy()
+
+
+def check_tickets_zero(workspace, what):
+    t = tickets(workspace)
+    assert not t.any(), f"{what}: work tickets not reset: {t.tolist()}"
 
 
 def oracle_chain(cfg, inp, topk_idx=None, topk_w=None, caps=None, identity=None,

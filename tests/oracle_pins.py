@@ -384,6 +384,54 @@ def pin_plan_equal_units_match_lpt():
         assert np.diff(b).max() == loads.max() == -(-T // P)
 
 
+def _routed_slots(idx: np.ndarray, E: int) -> np.ndarray:
+    """Routed slots per token, from the routing rules alone (an index in
+    [0, E) that no earlier slot of the row repeats), not from the layout."""
+    T, k = idx.shape
+    n = np.zeros(T, np.int64)
+    for t in range(T):
+        seen = set()
+        for e in idx[t]:
+            if 0 <= e < E and e not in seen:
+                n[t] += 1
+            seen.add(int(e))
+    return n
+
+
+def pin_plan_mixed_costs_vs_list_scheduler():
+    """Tokens of mixed cost (masked slots, whole rows masked, a block of
+    rows with every slot masked): cut each token's payload into equal-cost
+    units (one row read, one row per routed slot) and spread the units over
+    P cores with the least-loaded list scheduler of Section 6.2 -- every
+    core ends within one unit of A/P.  The plan keeps tokens whole, so each
+    of its parts must carry A/P units to within one token's cost, with the
+    costs counted from the routing rules, not from the layout under test."""
+    E, R, k = 64, 16, 8
+    rng = np.random.Generator(np.random.PCG64(77))
+    for case, (T, P) in enumerate(((3000, 64), (777, 13), (4096, 512), (50, 7))):
+        logits = rng.standard_normal((T, E)).astype(np.float32)
+        idx = np.argsort(-logits, axis=1, kind="stable")[:, :k].astype(np.int32)
+        idx[rng.random((T, k)) < 0.3] = -1       # scattered unused slots
+        idx[: T // 3] = -1                       # a third of the batch unrouted
+        idx[T // 2: T // 2 + 5, 1] = idx[T // 2: T // 2 + 5, 0]   # repeats
+        cost = 1 + _routed_slots(idx, E)
+        A = int(cost.sum())
+        # least-loaded list scheduling of A equal units onto P cores
+        loads = np.zeros(P, np.int64)
+        for _ in range(A):
+            loads[int(np.argmin(loads))] += 1
+        assert loads.max() - loads.min() <= 1 and loads.sum() == A
+        lay = oracle.layout(idx, E, R)
+        b = oracle.plan(lay["pos"], T, k, P).astype(np.int64)
+        assert b[0] == 0 and b[-1] == T and np.all(np.diff(b) >= 0), case
+        cp = np.concatenate([[0], np.cumsum(cost)])
+        part = cp[b[1:]] - cp[b[:-1]]
+        slack = int(cost.max()) - 1
+        assert part.max() <= loads.max() + slack, (case, part.max(), loads.max())
+        assert part.min() >= loads.min() - slack, (case, part.min(), loads.min())
+        assert part.sum() == A
+
+
 # ----------------------------------------------------------------- dispatch
 def _rows_u8(x):
     return np.ascontiguousarray(x).view(np.uint8).reshape(x.shape[0], -1)

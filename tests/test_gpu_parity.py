@@ -353,51 +353,26 @@ def test_decode_workload_full():
 
 @pytest.mark.parametrize("name", ["prefill", "fp8", "large"])
 def test_full_size_workloads(name):
-    """Full-size workloads: layout, plan and dispatch compared in full against
-    the oracle; combine checked end to end two ways: (1) unit weights on the
-    dispatched rows themselves give exactly bf16(k*x) for every token (bf16
-    payloads); (2) the scaled expert and softmax weights on a sample of
-    tokens, against the oracle chain run on that sample alone (a token's
-    output does not depend on the other tokens)."""
+    """Full-size workloads against the whole oracle chain: layout, plan,
+    dispatch and the stand-in expert bit-exact, and combine within the
+    tolerance on every token.  Dispatch and combine run twice on one layout
+    (at these sizes the default split claims parts at run time, so the
+    second call relies on the first one's counter reset; the outputs are
+    reset to the sentinel in between).  For bf16 payloads, unit weights on
+    the dispatched rows themselves must also give exactly bf16(k*x) for
+    every token."""
     h = _h()
     cfg = wl.get(name)
     inp = wl.make_inputs(cfg)
-    T, H, E, R, k = cfg["T"], cfg["H"], cfg["E"], cfg["R"], cfg["k"]
+    k = cfg["k"]
     h.log(f"[full] {cfg['name']}")
-    # two dispatch + combine calls on one layout: at these sizes the default
-    # split claims parts at run time, so the second call relies on the first
-    # one's counter reset
-    run = h.GpuRun(cfg, inp, spare_rows=1, repeat=2)
-    lay = oracle.layout(inp["topk_idx"], E, R)
-    for key in ("expert_count", "expert_offset", "rank_count", "rank_offset", "pos",
-                "row_src"):
-        assert np.array_equal(run.layout[key], lay[key]), key
-    assert np.array_equal(run.plan, oracle.plan(lay["pos"], T, k, len(run.plan) - 1))
+    run, ref = _full_parity(cfg, inp, spare_rows=1, repeat=2)
     assert run.layout["status"] == 0
-    fp8 = cfg["payload"] == wl.FP8_E4M3
-    xs = h.u8_rows(inp["x_scales"]) if fp8 else None
-    regs, sregs, st = oracle.dispatch(h.u8_rows(inp["x"]), xs, inp["topk_idx"], lay["pos"],
-                                      lay["rank_offset"], E, R, run.caps, h.SENTINEL,
-                                      scale_pitch=run.scale_pitch)
-    assert st == 0
-    h.check_regions(run, run.regions, regs)
-    if fp8:
-        h.check_regions(run, run.sregions, sregs)
-    del regs, sregs
-    h.log(f"[full] {cfg['name']} layout+plan+dispatch bit-exact")
+    h.log(f"[full] {cfg['name']}: layout, plan, dispatch, expert bit-exact; "
+          f"combine within tolerance on all {cfg['T']} tokens")
+    del ref
 
-    rng = np.random.Generator(np.random.PCG64(99))
-    sample = np.sort(rng.choice(T, size=min(T, 384), replace=False))
-    sub = dict(inp, topk_idx=inp["topk_idx"][sample], topk_w=inp["topk_w"][sample],
-               x=inp["x"][sample],
-               x_scales=inp["x_scales"][sample] if fp8 else None)
-    subcfg = dict(cfg, T=len(sample))
-    ref = h.oracle_chain(subcfg, sub, scale_pitch=run.scale_pitch)
-    ok, msg = h.combine_close(run.y[sample], ref["y"])
-    assert ok, msg
-    h.log(f"[full] {cfg['name']} sampled combine ok ({msg})")
-
-    if not fp8:
+    if cfg["payload"] != wl.FP8_E4M3:
         run1 = h.GpuRun(cfg, inp, topk_w=np.ones_like(inp["topk_w"]),
                         combine_on_dispatch=True)
         xf = (inp["x"].astype(np.uint32) << 16).view(np.float32) * np.float32(k)

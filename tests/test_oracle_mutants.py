@@ -46,6 +46,7 @@ MUTANTS = [
     ("fixed_window_reversed", "const int32_t p = e * C + expert_count[e];",
      "const int32_t p = e * C + (C - 1 - expert_count[e]);"),
     ("plan_cost_ignores_read", "int64_t c = 1;", "int64_t c = 0;"),
+    ("plan_counts_unused_slots", "c += pos[t * k + j] >= 0 ? 1 : 0;", "c += 1;"),
     ("plan_boundary_off_by_one", "a[(size_t)t] * P < p * A", "a[(size_t)t] * P <= p * A"),
     ("dispatch_short_copy", "x + t * row_bytes, (size_t)row_bytes);",
      "x + t * row_bytes, (size_t)row_bytes - 2);"),
