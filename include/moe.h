@@ -23,8 +23,13 @@
  * Conventions for every entry point:
  *  - All array arguments are DEVICE pointers unless marked "host".  The
  *    caller allocates and owns every buffer; the library allocates, frees
- *    and caches no memory.  It keeps no state between calls other than the
- *    device properties it reads once per device.
+ *    and caches no memory (moe_layout_scratch uses one fixed array of the
+ *    library's, see there).  Host-side it keeps only what it reads once per
+ *    device (device properties, that array's address).  Device-side, the
+ *    default work split of moe_dispatch / moe_combine hands parts out from
+ *    ticket counters in the caller's workspace, which every call leaves at
+ *    zero: calls that share a workspace must not overlap in time; separate
+ *    workspaces are independent.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Every call only enqueues kernels on `stream` and returns without
  *    synchronizing; outputs are ready when the stream reaches that point.
@@ -138,6 +143,39 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
                int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
                int32_t* rank_offset, int32_t* pos, int32_t* row_src, void* workspace,
                size_t workspace_bytes, uint32_t* status, void* stream);
+
+/*
+ * moe_layout_scratch -- moe_layout for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same kernels and the same outputs, but the
+ * workspace is the library's own, a fixed device array of 576 KiB per GPU
+ * (held until the process ends), large enough for every shape the library
+ * accepts (moe_layout_workspace_bytes never exceeds 573952 bytes).  This
+ * call allocates and frees nothing.
+ *
+ * In/out: as moe_layout, without the workspace arguments.
+ * workspace        HOST out: device address of the library's workspace on
+ *                  the current device; pass it, with *workspace_bytes, as
+ *                  the workspace of this batch's moe_dispatch / moe_combine
+ *                  (and moe_dispatch_ex, moe_combine_ex).  Its front holds
+ *                  the partition plan, as for moe_layout.
+ * workspace_bytes  HOST out: moe_layout_workspace_bytes for this shape.
+ * Every call on one GPU uses that GPU's one array and leaves its plan there
+ * until the next call: the batch's dispatch and combine must be enqueued
+ * before the next moe_layout_scratch on that GPU, and calls (this one, or
+ * the dispatch / combine that use its workspace) that overlap on one GPU --
+ * concurrent streams, other host threads -- race.  The first call on a
+ * device looks the array's address up (hipGetSymbolAddress); make that
+ * first call outside graph capture.
+ * Errors: as moe_layout (argument errors are found before any HIP call);
+ * MOE_EINVAL for null workspace / workspace_bytes; MOE_EWORKSPACE if a
+ * shape needed more than the array (none does); MOE_ELAUNCH if the address
+ * lookup fails.
+ */
+int moe_layout_scratch(const int32_t* topk_idx, int64_t T, int k, int E, int R,
+                       int32_t* expert_count, int32_t* expert_offset, int32_t* rank_count,
+                       int32_t* rank_offset, int32_t* pos, int32_t* row_src, uint32_t* status,
+                       void** workspace, size_t* workspace_bytes, void* stream);
 
 /*
  * moe_layout_fixed -- token placement into fixed-capacity expert windows:

@@ -19,7 +19,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libmoe.so")
-SOURCES = ["api.hip", "layout.hip", "dispatch.hip", "combine.hip", "expert.hip", "dedup.hip"]
+SOURCES = ["api.hip", "layout.hip", "dispatch.hip", "combine.hip", "expert.hip", "dedup.hip",
+           "scratch.hip"]
 
 
 def hipcc() -> str:

@@ -73,15 +73,17 @@ int shape_ok(int64_t T, int k, int E, int R) {
   return MOE_OK;
 }
 
-int launched(hipError_t err) {
-  if (err == hipSuccess) return MOE_OK;
-  g_last_hip_error = (int)err;
-  return MOE_ELAUNCH;
-}
+int launched(hipError_t err) { return moe::hip_status(err); }
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 }  // namespace
+
+int moe::hip_status(hipError_t err) {
+  if (err == hipSuccess) return MOE_OK;
+  g_last_hip_error = (int)err;
+  return MOE_ELAUNCH;
+}
 
 extern "C" {
 

@@ -35,6 +35,10 @@ struct LayoutGeom {
 
 LayoutGeom layout_geom(int64_t T, int E);
 
+// MOE_OK for hipSuccess; otherwise records the error for
+// moe_last_hip_error() and returns MOE_ELAUNCH.
+int hip_status(hipError_t err);
+
 // Slot width the layout kernels are compiled for: smallest of 2, 4, 8, 16,
 // 32 that is >= k.
 int slot_width(int k);

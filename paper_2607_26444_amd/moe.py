@@ -45,7 +45,7 @@ EXPORTS = ("moe_version", "moe_strerror", "moe_last_hip_error", "moe_wall_clock_
            "moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
            "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale",
            "moe_layout_dedup_workspace_bytes", "moe_layout_dedup", "moe_dispatch_dedup",
-           "moe_expand", "moe_combine_local", "moe_combine_dedup")
+           "moe_expand", "moe_combine_local", "moe_combine_dedup", "moe_layout_scratch")
 
 _lib = None
 P = ctypes.c_void_p
@@ -99,7 +99,9 @@ def lib() -> ctypes.CDLL:
         L.moe_combine_local.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, P, P,
                                         P, SZ, P, P]
         L.moe_combine_dedup.argtypes = [P, I64, I32, I32, I32, I32, P, P, P, P, P, P, SZ, P, P]
-        for f in ("moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
+        L.moe_layout_scratch.argtypes = [P, I64, I32, I32, I32, P, P, P, P, P, P, P,
+                                         ctypes.POINTER(P), ctypes.POINTER(SZ), P]
+        for f in ("moe_layout_scratch", "moe_layout_workspace_bytes", "moe_layout", "moe_layout_fixed", "moe_dispatch",
                   "moe_dispatch_ex", "moe_combine", "moe_combine_ex", "moe_expert_scale",
                   "moe_layout_dedup_workspace_bytes", "moe_layout_dedup", "moe_dispatch_dedup",
                   "moe_expand", "moe_combine_local", "moe_combine_dedup"):
@@ -150,6 +152,38 @@ def moe_layout(topk_idx, E, R, expert_count, expert_offset, rank_count, rank_off
         _ptr(topk_idx), T, k, E, R, _ptr(expert_count), _ptr(expert_offset),
         _ptr(rank_count), _ptr(rank_offset), _ptr(pos), _ptr(row_src), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(status), _stream(stream)))
+
+
+class DeviceBuffer:
+    """A device address and size the library owns (the workspace that
+    moe_layout_scratch returns), passed where the bindings take a tensor."""
+
+    is_cuda = True
+
+    def __init__(self, ptr: int, nbytes: int):
+        self.ptr, self.nbytes = int(ptr), int(nbytes)
+
+    def data_ptr(self) -> int:
+        return self.ptr
+
+    def numel(self) -> int:
+        return self.nbytes
+
+    def element_size(self) -> int:
+        return 1
+
+
+def moe_layout_scratch(topk_idx, E, R, expert_count, expert_offset, rank_count, rank_offset,
+                       pos, row_src, status, stream=None) -> DeviceBuffer:
+    """moe_layout into the library's own workspace; returns that workspace
+    for this batch's dispatch and combine."""
+    T, k = topk_idx.shape
+    ws, nbytes = P(), SZ(0)
+    _check("moe_layout_scratch", lib().moe_layout_scratch(
+        _ptr(topk_idx), T, k, E, R, _ptr(expert_count), _ptr(expert_offset),
+        _ptr(rank_count), _ptr(rank_offset), _ptr(pos), _ptr(row_src), _ptr(status),
+        ctypes.byref(ws), ctypes.byref(nbytes), _stream(stream)))
+    return DeviceBuffer(ws.value, nbytes.value)
 
 
 def moe_layout_fixed(topk_idx, E, R, capacity, expert_count, expert_offset, rank_count,

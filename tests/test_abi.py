@@ -206,3 +206,27 @@ def test_dedup_argument_errors():
     assert L.moe_combine_dedup(*bad) == moe.MOE_EWORKSPACE
     bad = list(s); bad[0] = None
     assert L.moe_combine_dedup(*bad) == moe.MOE_EINVAL
+
+
+def test_layout_scratch_argument_errors():
+    """moe_layout_scratch rejects bad arguments before any HIP call."""
+    L = moe.lib()
+    ws, nb = ctypes.c_void_p(), ctypes.c_size_t()
+    ok = [FAKE, 64, 8, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+          ctypes.byref(ws), ctypes.byref(nb), None]
+    for i, v in ((12, None), (13, None), (5, None), (11, None), (9, None), (3, 48), (1, -1),
+                 (2, 33)):
+        bad = list(ok)
+        bad[i] = v
+        assert L.moe_layout_scratch(*bad) == moe.MOE_EINVAL, i
+
+
+def test_layout_scratch_array_covers_every_shape():
+    """The library's workspace array (576 KiB) holds the workspace of every
+    accepted shape: the count matrix is largest for E = 1 at the largest T."""
+    sizes = [moe.moe_layout_workspace_bytes(2 ** 31 - 1, 1, E, 1) for E in range(1, 1025)]
+    assert max(sizes) == 573952 == sizes[0]
+    assert max(sizes) <= 576 * 1024
+    for T in (0, 1, 255, 256, 257, 4096, 16384, 2 ** 20):
+        for E in (1, 3, 16, 256, 1024):
+            assert moe.moe_layout_workspace_bytes(T, 1, E, 1) <= 576 * 1024
