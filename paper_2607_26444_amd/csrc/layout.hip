@@ -170,6 +170,9 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   int32_t* base = reinterpret_cast<int32_t*>(scan + kWavesPerBlock);  // [E]
   int32_t* eoff = base + E;                                         // [E+1]
   int32_t* woff = eoff + E + 1;  // [4][E]; before placement, 2 x [groups][ncp] count partials
+  // token (within the sub-chunk) of each cost unit of the sub-chunk
+  uint16_t* owner = reinterpret_cast<uint16_t*>(
+      woff + (kWavesPerBlock * E > 8 * kBlock ? kWavesPerBlock * E : 8 * kBlock));
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const int c = blockIdx.x;
@@ -362,16 +365,21 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       }
     }
     // Plan boundaries inside this sub-chunk: token t owns the parts p with
-    // a_t*P < p*A <= (a_t + cost_t)*P, each starting at token t+1.
+    // a_t*P < p*A <= (a_t + cost_t)*P, each starting at token t+1.  In cost
+    // units, part p starts inside unit ceil(p*A/P) - 1, so the sub-chunk's
+    // units are mapped to their tokens in LDS and the parts are written
+    // part-major: lane l of each store takes part p0 + l (coalesced; a token
+    // may own hundreds of parts when there are few tokens).
     const int64_t cost = (t < c1) ? 1 + nplaced : 0;
     int64_t sub_total = 0;
-    const int64_t a = cost_base + block_exclusive_scan(cost, scan, sub_total);
-    if (cost) {
-      const int64_t p_lo = (a * P) / A + 1, p_hi = ((a + cost) * P) / A;
-      for (int64_t p = p_lo; p <= p_hi; ++p) bound[p] = (int32_t)(t + 1);
-    }
-    cost_base += sub_total;
+    const int64_t ex = block_exclusive_scan(cost, scan, sub_total);
+    for (int64_t u = ex; u < ex + cost; ++u) owner[u] = (uint16_t)tid;
     __syncthreads();
+    const int64_t p_first = (cost_base * P) / A + 1;
+    const int64_t p_last = ((cost_base + sub_total) * P) / A;
+    for (int64_t p = p_first + tid; p <= p_last; p += kBlock)
+      bound[p] = (int32_t)(s0 + owner[(p * A - 1) / P - cost_base] + 1);
+    cost_base += sub_total;
     for (int i = tid; i < kWavesPerBlock * E; i += kBlock) mask[i] = 0;
     __syncthreads();
   }
@@ -408,7 +416,8 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int pee
   const size_t woff_ints = (size_t)kWavesPerBlock * E > 8 * kBlock ? (size_t)kWavesPerBlock * E
                                                                     : 8 * kBlock;
   const size_t lds_place = (size_t)kWavesPerBlock * E * 8 + kWavesPerBlock * 8 +
-                           (size_t)E * 4 + (size_t)(E + 1) * 4 + woff_ints * 4;
+                           (size_t)E * 4 + (size_t)(E + 1) * 4 + woff_ints * 4 +
+                           (size_t)kBlock * (1 + KW) * 2;
   if (g.nc == 1 && T <= kBlock) {
     hipLaunchKernelGGL((layout_place_kernel<KW, true, FIXED>), dim3(1), dim3(kBlock), lds_place,
                        stream, idx, T, k, E, peer_L, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
