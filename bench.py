@@ -111,9 +111,59 @@ def algorithmic_bytes(cfg) -> dict:
     fp8 = cfg["payload"] == 1
     row = H * (1 if fp8 else 2) + ((H // 128) * 4 if fp8 else 0)
     n = T * k
-    dispatch = T * row + n * row + 4 * n
-    combine = n * 2 * H + 8 * n + T * 2 * H
-    return dict(dispatch=dispatch, combine=combine, row=row, n=n)
+    d_read, d_write = T * row + 4 * n, n * row
+    c_read, c_write = n * 2 * H + 8 * n, T * 2 * H
+    return dict(dispatch=d_read + d_write, combine=c_read + c_write, row=row, n=n,
+                dispatch_read=d_read, dispatch_write=d_write,
+                combine_read=c_read, combine_write=c_write)
+
+
+def stream_ceiling(read_bytes, write_bytes, read_GBps, write_GBps):
+    """GB/s of a kernel that reads read_bytes and writes write_bytes if its
+    reads ran at the pure-read rate and its writes at the pure-write rate,
+    one after the other.  Mixing the two in one stream only adds read/write
+    turnarounds, so this bounds what a mixed kernel can reach."""
+    t = read_bytes / read_GBps + write_bytes / write_GBps
+    return (read_bytes + write_bytes) / t if t > 0 else float("nan")
+
+
+def measure_stream_legs(dev, stream, read_bytes, write_bytes, reps=10):
+    """Pure-write and pure-read rates on this GPU, built from torch ops (no
+    kernel of this library): fill_ of a buffer of write_bytes, and a float32
+    sum and an int32 max over a buffer of read_bytes (the faster of the two
+    counts).  GB/s of the bytes each op moves."""
+    import torch
+    out = {}
+    buf = torch.empty(max(1 << 20, write_bytes // 16 * 16), dtype=torch.uint8, device=dev)
+    for i in range(3):
+        buf.fill_(i)
+    e0, e1 = Event(), Event()
+    e0.record(stream)
+    for i in range(reps):
+        buf.fill_(i & 0xFF)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    out["write_GBps"] = buf.numel() * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    out["write_buffer_bytes"] = buf.numel()
+    del buf
+    buf = torch.zeros(max(1 << 20, read_bytes // 16 * 16), dtype=torch.uint8, device=dev)
+    rates = {}
+    for name, op in (("sum_f32", lambda b: b.view(torch.float32).sum()),
+                     ("max_i32", lambda b: b.view(torch.int32).amax())):
+        for _ in range(3):
+            op(buf)
+        e0.record(stream)
+        for _ in range(reps):
+            op(buf)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        rates[name] = buf.numel() * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    out["read_op"] = max(rates, key=rates.get)
+    out["read_GBps"] = rates[out["read_op"]]
+    out["read_rates_GBps"] = {n: round(v, 1) for n, v in rates.items()}
+    out["read_buffer_bytes"] = buf.numel()
+    del buf
+    return out
 
 
 def kernel_source_hash(kernel: str) -> str:
@@ -796,6 +846,26 @@ def main(argv=None):
     out["hbm_copy_equal_bytes_GBps"] = round(2 * half * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9,
                                              1)
     del src, dst
+
+    # Measured ceiling: what pure writes (dispatch's write bytes) and pure
+    # reads (combine's read bytes) sustain on this GPU, and the rate each
+    # kernel would reach with its reads and writes at those rates.
+    legs = measure_stream_legs(dev, stream, b["combine_read"], b["dispatch_write"])
+    ceil_d = stream_ceiling(b["dispatch_read"], b["dispatch_write"], legs["read_GBps"],
+                            legs["write_GBps"])
+    ceil_c = stream_ceiling(b["combine_read"], b["combine_write"], legs["read_GBps"],
+                            legs["write_GBps"])
+    out["ceiling"] = {
+        "write_GBps": round(legs["write_GBps"], 1), "write_op": "torch fill_ (uint8)",
+        "write_buffer_bytes": legs["write_buffer_bytes"],
+        "read_GBps": round(legs["read_GBps"], 1), "read_op": legs["read_op"],
+        "read_rates_GBps": legs["read_rates_GBps"], "read_buffer_bytes": legs["read_buffer_bytes"],
+        "dispatch_GBps": round(ceil_d, 1), "combine_GBps": round(ceil_c, 1),
+        "dispatch_frac": _num(d_gbps / ceil_d, 4), "combine_frac": _num(c_gbps / ceil_c, 4)}
+    if graph is None:
+        ach = ceil_d if dom == "dispatch" else ceil_c
+        out["roofline"]["achievable"] = round(ach, 1)
+        out["roofline"]["frac_of_achievable"] = round(achieved / ach, 4)
 
     if not a.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

@@ -50,7 +50,10 @@
  *    one token's row: later repeats are treated as unused),
  *    MOE_STATUS_CAPACITY (a row's region-local index is outside
  *    [0, recv_cap[r]): dispatch does not write it and combine does not read
- *    it; a negative index only arises when pos does not belong to topk_idx).
+ *    it; a negative index only arises when pos does not belong to topk_idx),
+ *    MOE_STATUS_LAYOUT_SYNC (the layout's workgroups did not all reach its
+ *    grid barrier within 2 s -- other work held the compute units that long;
+ *    that call's outputs are not valid).
  *  - The three calls of one batch must see the same topk_idx, T, k, E, R and
  *    workspace; dispatch and combine read the partition plan that moe_layout
  *    leaves in the workspace.
@@ -65,7 +68,7 @@
 extern "C" {
 #endif
 
-#define MOE_VERSION 4
+#define MOE_VERSION 5
 
 #define MOE_OK 0
 #define MOE_EINVAL (-1)
@@ -79,6 +82,7 @@ extern "C" {
 #define MOE_STATUS_BAD_INDEX 1u
 #define MOE_STATUS_DUP_INDEX 2u
 #define MOE_STATUS_CAPACITY 4u
+#define MOE_STATUS_LAYOUT_SYNC 8u
 
 #define MOE_MAX_K 32
 #define MOE_MAX_EXPERTS 1024
@@ -135,7 +139,15 @@ int moe_layout_workspace_bytes(int64_t T, int k, int E, int R, size_t* out_bytes
  *      row_src[T*k]         inverse map: slot index t*k+j of global row i for
  *                           i < N, -1 for i >= N;
  *      workspace            partition plan (see above) + scratch;
- *      status               OR-ed bits (BAD_INDEX, DUP_INDEX).
+ *      status               OR-ed bits (BAD_INDEX, DUP_INDEX, LAYOUT_SYNC).
+ * Launches: one workgroup when T <= 256; one launch whose workgroups (one
+ * per 256-token chunk, at most 32) meet at a grid barrier when the batch
+ * fits that; a counting launch and a placing launch otherwise.  The barrier
+ * needs no cleared memory: the workspace holds a generation word that each
+ * such call advances on the device, and a workgroup's arrival flag carries a
+ * 64-bit hash of it, which leftover memory matches only by chance (2^-64).
+ * The workspace may therefore be uninitialised, reused across shapes, or
+ * used from a replayed graph.
  * Results are deterministic and bit-identical from run to run.  T = 0 is
  * allowed (counts and offsets become 0).
  */

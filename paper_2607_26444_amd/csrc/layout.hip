@@ -34,6 +34,10 @@
 // out one row per (token, peer) pair: E is then the number of peers and
 // load_row bins the expert indices by peer as it reads them.
 
+#include <map>
+#include <mutex>
+#include <tuple>
+
 #include "moe_internal.h"
 
 namespace moe {
@@ -82,29 +86,46 @@ __device__ __forceinline__ void load_row(const int32_t* __restrict__ idx, int64_
   }
 }
 
-// Exclusive scan of one int64 per thread over the 256-thread block; also
-// returns the block total.  `scratch` holds kWavesPerBlock int64.
-__device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* scratch,
-                                                        int64_t& total) {
+// Inclusive scan over the 64 lanes of a wavefront with gfx9 DPP row shifts
+// (within rows of 16 lanes) and row broadcasts (lane 15 into rows 1 and 3,
+// then lane 31 into rows 2 and 3).  Lanes a step does not feed add 0.  The
+// operands move through the vector ALU, not through LDS as a shuffle does.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
+// Exclusive scans of two uint32 per thread over the 256-thread block (ea,
+// eb) and their block totals (ta, tb); the sums must stay below 2^32.
+// `scratch` holds 2 * kWavesPerBlock uint32.
+__device__ __forceinline__ void block_exclusive_scan2(uint32_t a, uint32_t b, uint32_t* scratch,
+                                                      uint32_t& ea, uint32_t& eb, uint32_t& ta,
+                                                      uint32_t& tb) {
   const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
-  int64_t inc = v;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const int64_t o = __shfl_up(inc, d, kWave);
-    if (lane >= d) inc += o;
+  const uint32_t ia = wave_inclusive_scan(a), ib = wave_inclusive_scan(b);
+  if (lane == kWave - 1) {
+    scratch[w] = ia;
+    scratch[kWavesPerBlock + w] = ib;
   }
-  if (lane == kWave - 1) scratch[w] = inc;
   __syncthreads();
-  int64_t before = 0;
-  total = 0;
+  uint32_t ba = 0, bb = 0;
+  ta = tb = 0;
 #pragma unroll
   for (int i = 0; i < kWavesPerBlock; ++i) {
-    const int64_t s = scratch[i];
-    before += (i < w) ? s : 0;
-    total += s;
+    const uint32_t sa = scratch[i], sb = scratch[kWavesPerBlock + i];
+    ba += (i < w) ? sa : 0u;
+    bb += (i < w) ? sb : 0u;
+    ta += sa;
+    tb += sb;
   }
   __syncthreads();
-  return before + inc - v;
+  ea = ba + ia - a;
+  eb = bb + ib - b;
 }
 
 template <int KW>
@@ -151,19 +172,108 @@ constexpr int kMaxExpertsPerThread = MOE_MAX_EXPERTS / kBlock;  // 4
 constexpr int kCountBatch = 16;      // 16-byte count loads in flight per thread
 constexpr int kMaxCountGroups = 16;  // count-matrix rows read side by side
 
-// SINGLE: the whole batch is one sub-chunk (T <= kBlock), so this kernel
-// also does the counting (no layout_count launch): the totals are the
-// popcounts of its own bitmaps.
+// How layout_place_kernel learns the per-chunk counts.
+//   kPlaceAfterCount  a layout_count launch left the count matrix
+//   kPlaceSingle      one workgroup holds the whole batch (T <= kBlock): the
+//                     totals are the popcounts of its own bitmaps
+//   kPlaceFused       every workgroup counts its chunk (one sub-chunk of
+//                     kBlock tokens), publishes its count row, and waits at a
+//                     grid barrier until every row is published; one launch
+//                     instead of two, and the bitmaps built for counting are
+//                     reused for placement
+constexpr int kPlaceAfterCount = 0;
+constexpr int kPlaceSingle = 1;
+constexpr int kPlaceFused = 2;
+
+// Grid barrier of the fused layout without a counter in a known state: the
+// workspace holds a generation word and one arrival flag per chunk.  Every
+// workgroup reads the generation g at entry and publishes its count row
+// with flag = mix(g), then waits until all flags equal mix(g); workgroup 0
+// then stores mix(g) as the next generation.  mix is a 64-bit bijection with
+// good avalanche (the SplitMix64 finalizer, after adding an odd constant so
+// that 0 does not map to 0), so a flag left over from a previous call holds
+// an earlier generation's value and cannot match, and memory that was never
+// a workspace matches only by a 2^-64 coincidence.  Every call advances the
+// word on the device, so a call replayed from a captured graph gets a fresh
+// value as well.
+__device__ __forceinline__ uint64_t sync_epoch(uint64_t g) {
+  uint64_t z = g + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Writes the plan boundaries bound[p] for p in [p_first, p_last], the parts
+// that start inside a sub-chunk whose cost units begin at cost_base: part p
+// starts at the token after the owner of unit ceil(p*A/P) - 1 (owner[] maps
+// the sub-chunk's n_units units to token offsets from s0).  Thread i takes the
+// four-part groups i, i + 256, i + 512, ... of the range, so neighbouring
+// lanes store neighbouring 16 bytes.  The unit of a part is kept as the
+// quotient and remainder of p*A - 1 by P: one division for the thread's
+// first group, then steps by A (next part) and by 1024*A (next group of the
+// thread), so a single workgroup writing all P + 1 boundaries does no
+// division per part.
+__device__ __forceinline__ void write_plan(int32_t* __restrict__ bound, int64_t p_first,
+                                           int64_t p_last, int64_t A, int64_t cost_base,
+                                           int64_t n_units, const uint16_t* owner, int64_t s0) {
+  constexpr int64_t P = MOE_PLAN_PARTS;
+  constexpr int64_t kStride = 4 * kBlock;    // parts between a thread's groups
+  const int64_t q0 = (p_first >> 2) + threadIdx.x;
+  if (q0 > (p_last >> 2)) return;
+  const int64_t qA = A / P, rA = A - qA * P;
+  const int64_t sA = kStride * A;
+  const int64_t qS = sA / P, rS = sA - qS * P;
+  // (u, r): floor quotient and remainder of 4q*A - 1 by P for the group's
+  // first part p0 = 4q (p0 = 0 gives -1: u = -1, r = P - 1)
+  const int64_t n0 = 4 * q0 * A - 1;
+  int64_t u = n0 >= 0 ? n0 / P : -1;
+  int64_t r = n0 - u * P;
+  for (int64_t q = q0; q <= (p_last >> 2); q += kBlock) {
+    const int64_t p0 = q * 4;
+    int v[4];
+    int64_t uu = u, rr = r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      // unconditional (clamped) lookup: the four LDS reads go out together
+      const int64_t ui = min(max(uu - cost_base, (int64_t)0), n_units - 1);
+      v[i] = (int)(s0 + owner[ui] + 1);
+      uu += qA;
+      rr += rA;
+      if (rr >= P) {
+        rr -= P;
+        ++uu;
+      }
+    }
+    if (p0 >= p_first && p0 + 3 <= p_last) {
+      *reinterpret_cast<int4*>(bound + p0) = int4{v[0], v[1], v[2], v[3]};
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (p0 + i >= p_first && p0 + i <= p_last) bound[p0 + i] = v[i];
+    }
+    u += qS;
+    r += rS;
+    if (r >= P) {
+      r -= P;
+      ++u;
+    }
+  }
+}
+
 // FIXED: fixed-capacity windows of C rows per expert (expert e's window
 // starts at e*C); a slot whose rank within its expert reaches C is dropped.
-template <int KW, bool SINGLE, bool FIXED>
+// MODE kPlaceFused: gen, flags and sync_ticks (the barrier's time limit in
+// wall-clock ticks; past it the status word gets MOE_STATUS_LAYOUT_SYNC) as
+// described at sync_epoch; the counts pointer is then written as well.
+template <int KW, int MODE, bool FIXED>
 __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     const int32_t* __restrict__ idx, int64_t T, int k, int E, int peer_L, int R, int C,
-    int64_t chunk_tokens, int nc, int ncp, const int32_t* __restrict__ counts, int32_t* __restrict__ expert_count,
+    int64_t chunk_tokens, int nc, int ncp, int32_t* counts, int32_t* __restrict__ expert_count,
     int32_t* __restrict__ expert_offset, int32_t* __restrict__ rank_count,
     int32_t* __restrict__ rank_offset, int32_t* __restrict__ pos,
     int32_t* __restrict__ row_src, int32_t* __restrict__ bound, uint32_t* __restrict__ tickets,
-    uint32_t* __restrict__ status) {
+    uint32_t* __restrict__ status, uint64_t* gen, uint64_t* flags, uint64_t sync_ticks) {
+  constexpr bool SINGLE = MODE == kPlaceSingle;
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* mask = reinterpret_cast<uint64_t*>(smem);               // [4][E]
   int64_t* scan = reinterpret_cast<int64_t*>(mask + kWavesPerBlock * E);  // [4]
@@ -194,12 +304,58 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   // scan over experts).
   const int ept = (E + kBlock - 1) / kBlock;
   int tot[kMaxExpertsPerThread], pre[kMaxExpertsPerThread];
-  if (SINGLE) {
+  if (MODE != kPlaceAfterCount) {
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < KW; ++j)
       if (ok0[j]) atomicOr(&mask[w * E + ev0[j]], 1ull << lane);
     __syncthreads();
+  }
+  if constexpr (MODE == kPlaceFused) {
+    // Publish this chunk's count row, then wait for every chunk's.
+    // Wave 0 alone writes the row and synchronizes, so one cache write-back
+    // (release) and one invalidate (acquire) per workgroup suffice: on
+    // MI355X each costs a serialized L2 operation, and with one per wave the
+    // barrier took twice as long.
+    if (w == 0) {
+      const uint64_t epoch =
+          sync_epoch(__hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      for (int e = lane; e < E; e += kWave) {
+        int cnt = 0;
+#pragma unroll
+        for (int q = 0; q < kWavesPerBlock; ++q) cnt += __popcll(mask[q * E + e]);
+        counts[(int64_t)c * ncp + e] = cnt;
+      }
+      if (lane == 0)
+        __hip_atomic_store(flags + c, epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t t_begin = (uint64_t)wall_clock64();
+      for (;;) {
+        bool here = true;   // all flags this lane checks (loads issued together)
+#pragma unroll
+        for (int r = 0; r < (kMaxSyncChunks + kWave - 1) / kWave; ++r) {
+          const int i = lane + r * kWave;
+          if (i < nc)
+            here &= __hip_atomic_load(flags + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                    epoch;
+        }
+        if (__all(here)) break;
+        if ((uint64_t)wall_clock64() - t_begin > sync_ticks) {
+          st |= MOE_STATUS_LAYOUT_SYNC;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      // every workgroup read the generation before it published its flag
+      if (c == 0 && lane == 0)
+        __hip_atomic_store(gen, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // The other waves read the count matrix after this barrier, ordered
+    // behind wave 0's acquire (which also invalidated this compute unit's
+    // caches).
+    __syncthreads();
+  }
+  if (SINGLE) {
 #pragma unroll
     for (int q = 0; q < kMaxExpertsPerThread; ++q) {
       tot[q] = pre[q] = 0;
@@ -264,13 +420,13 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     my_tot += FIXED ? min(tot[q], C) : tot[q];
     my_pre += FIXED ? min(pre[q], C) : pre[q];
   }
-  // One scan for both sums: totals in the high 32 bits, this chunk's prefix
-  // in the low 32 (all sums are below 2^31, so no carry crosses).
-  int64_t packed_total = 0;
-  const int64_t packed = block_exclusive_scan((my_tot << 32) | my_pre, scan, packed_total);
-  int64_t run = packed >> 32;                      // rows before my experts
-  const int64_t n_total = packed_total >> 32;       // placed rows N
-  const int64_t pre_total = packed_total & 0xFFFFFFFFll;  // placed rows before chunk
+  // Both sums are below 2^31 (T * k is).
+  uint32_t ex_tot, ex_pre, sum_tot, sum_pre;
+  block_exclusive_scan2((uint32_t)my_tot, (uint32_t)my_pre, reinterpret_cast<uint32_t*>(scan),
+                        ex_tot, ex_pre, sum_tot, sum_pre);
+  int64_t run = ex_tot;                   // rows before my experts
+  const int64_t n_total = sum_tot;        // placed rows N
+  const int64_t pre_total = sum_pre;      // placed rows before chunk
   // base[e]: window start of expert e (prefix sum, or e*C) plus its rows in
   // earlier chunks; in fixed windows `base - e*C` is the rank within e.
   // eoff[e]: rows placed before expert e (its packed offset), for rank_count.
@@ -324,7 +480,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       uint32_t st_more = 0;
       load_row<KW>(idx, t, c1, k, E, peer_L, ev, ok, st_more);
     }
-    if (!SINGLE) {
+    if (MODE == kPlaceAfterCount) {
 #pragma unroll
       for (int j = 0; j < KW; ++j)
         if (ok[j]) atomicOr(&mask[w * E + ev[j]], 1ull << lane);
@@ -345,40 +501,59 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     }
     __syncthreads();
     const uint64_t below = (1ull << lane) - 1ull;
-    int nplaced = 0;
+    // Every slot's LDS lookups are issued before any is used (unused slots
+    // read expert 0's entries and ignore them): behind a per-slot branch
+    // each lookup would wait out its own LDS round trip.
+    int rank[KW];
 #pragma unroll
     for (int j = 0; j < KW; ++j) {
-      if (t < c1 && j < k) {
-        int p = -1;
-        if (ok[j]) {
-          const int e = ev[j];
-          const int r = woff[w * E + e] + __popcll(mask[w * E + e] & below);
-          if (!FIXED || r - e * C < C) {
-            p = r;
-            row_src[p] = (int32_t)(t * k + j);
-            ++nplaced;
-          } else {
-            st |= MOE_STATUS_CAPACITY;
-          }
+      const int e = ok[j] ? ev[j] : 0;
+      rank[j] = woff[w * E + e] + __popcll(mask[w * E + e] & below);
+    }
+    int nplaced = 0;
+    int pv[KW];
+#pragma unroll
+    for (int j = 0; j < KW; ++j) {
+      pv[j] = -1;
+      if (t < c1 && ok[j]) {
+        const int r = rank[j];
+        if (!FIXED || r - ev[j] * C < C) {
+          pv[j] = r;
+          row_src[r] = (int32_t)(t * k + j);
+          ++nplaced;
+        } else {
+          st |= MOE_STATUS_CAPACITY;
         }
-        pos[t * k + j] = p;
+      }
+    }
+    if (t < c1) {
+      if (k == KW && KW >= 4 && (reinterpret_cast<uintptr_t>(pos) & 15) == 0) {
+        // the token's k positions as 16-byte stores
+#pragma unroll
+        for (int j = 0; j < KW; j += 4)
+          *reinterpret_cast<int4*>(pos + t * k + j) = int4{pv[j], pv[j + 1], pv[j + 2], pv[j + 3]};
+      } else {
+#pragma unroll
+        for (int j = 0; j < KW; ++j)
+          if (j < k) pos[t * k + j] = pv[j];
       }
     }
     // Plan boundaries inside this sub-chunk: token t owns the parts p with
     // a_t*P < p*A <= (a_t + cost_t)*P, each starting at token t+1.  In cost
     // units, part p starts inside unit ceil(p*A/P) - 1, so the sub-chunk's
     // units are mapped to their tokens in LDS and the parts are written
-    // part-major: lane l of each store takes part p0 + l (coalesced; a token
-    // may own hundreds of parts when there are few tokens).
+    // part-major, four neighbouring parts per thread (coalesced; a token may
+    // own hundreds of parts when there are few tokens).
     const int64_t cost = (t < c1) ? 1 + nplaced : 0;
-    int64_t sub_total = 0;
-    const int64_t ex = block_exclusive_scan(cost, scan, sub_total);
+    uint32_t ex32, unused_e, sub32, unused_t;
+    block_exclusive_scan2((uint32_t)cost, 0u, reinterpret_cast<uint32_t*>(scan), ex32, unused_e,
+                          sub32, unused_t);
+    const int64_t ex = ex32, sub_total = sub32;
     for (int64_t u = ex; u < ex + cost; ++u) owner[u] = (uint16_t)tid;
     __syncthreads();
     const int64_t p_first = (cost_base * P) / A + 1;
     const int64_t p_last = ((cost_base + sub_total) * P) / A;
-    for (int64_t p = p_first + tid; p <= p_last; p += kBlock)
-      bound[p] = (int32_t)(s0 + owner[(p * A - 1) / P - cost_base] + 1);
+    write_plan(bound, p_first, p_last, A, cost_base, sub_total, owner, s0);
     cost_base += sub_total;
     for (int i = tid; i < kWavesPerBlock * E; i += kBlock) mask[i] = 0;
     __syncthreads();
@@ -400,6 +575,36 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
   if (lane == 0 && st) atomicOr(status, st);
 }
 
+// Workgroups of the fused layout that the current device keeps resident at
+// once (compute units x resident workgroups per unit for this LDS size),
+// queried once per (device, kernel, LDS bytes).  The grid barrier needs every
+// workgroup resident.
+int resident_blocks(const void* kernel, size_t lds_bytes) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, const void*, size_t>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_tuple(dev, kernel, lds_bytes);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int cus = 0, blocks = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, kBlock, lds_bytes) !=
+          hipSuccess)
+    cus = blocks = 0;
+  return cache[key] = cus * blocks;
+}
+
+// Time limit of the fused layout's grid barrier in wall-clock ticks (2 s).
+uint64_t sync_limit_ticks() {
+  int dev = 0, khz = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz < 1)
+    khz = 100000;
+  return (uint64_t)khz * 2000u;
+}
+
 template <int KW, bool FIXED>
 hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int peer_L, int R, int C,
                             int32_t* expert_count, int32_t* expert_offset,
@@ -407,9 +612,12 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int pee
                             int32_t* row_src, void* workspace, uint32_t* status,
                             hipStream_t stream) {
   const LayoutGeom g = layout_geom(T, E);
-  int32_t* bound = reinterpret_cast<int32_t*>(workspace);
-  int32_t* counts = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + g.counts_offset);
-  uint32_t* tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + g.ticket_offset);
+  char* ws = static_cast<char*>(workspace);
+  int32_t* bound = reinterpret_cast<int32_t*>(ws);
+  int32_t* counts = reinterpret_cast<int32_t*>(ws + g.counts_offset);
+  uint32_t* tickets = reinterpret_cast<uint32_t*>(ws + g.ticket_offset);
+  uint64_t* gen = reinterpret_cast<uint64_t*>(ws + g.gen_offset);
+  uint64_t* flags = g.sync_offset ? reinterpret_cast<uint64_t*>(ws + g.sync_offset) : nullptr;
   const size_t lds_count = (size_t)kWavesPerBlock * E * 8 + (size_t)E * 4;
   // woff also holds the two [groups][ncp] count partials (groups * ncp <=
   // 4 * kBlock int32 each) before placement starts.
@@ -419,22 +627,29 @@ hipError_t launch_layout_kw(const int32_t* idx, int64_t T, int k, int E, int pee
                            (size_t)E * 4 + (size_t)(E + 1) * 4 + woff_ints * 4 +
                            (size_t)kBlock * (1 + KW) * 2;
   if (g.nc == 1 && T <= kBlock) {
-    hipLaunchKernelGGL((layout_place_kernel<KW, true, FIXED>), dim3(1), dim3(kBlock), lds_place,
-                       stream, idx, T, k, E, peer_L, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
-                       expert_count,
-                       expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
-                       status);
+    hipLaunchKernelGGL((layout_place_kernel<KW, kPlaceSingle, FIXED>), dim3(1), dim3(kBlock),
+                       lds_place, stream, idx, T, k, E, peer_L, R, C, g.chunk_tokens, g.nc,
+                       g.ncp, counts, expert_count, expert_offset, rank_count, rank_offset, pos,
+                       row_src, bound, tickets, status, gen, flags, (uint64_t)0);
+    return hipGetLastError();
+  }
+  const void* fused = reinterpret_cast<const void*>(&layout_place_kernel<KW, kPlaceFused, FIXED>);
+  if (flags && g.nc <= resident_blocks(fused, lds_place)) {
+    hipLaunchKernelGGL((layout_place_kernel<KW, kPlaceFused, FIXED>), dim3(g.nc), dim3(kBlock),
+                       lds_place, stream, idx, T, k, E, peer_L, R, C, g.chunk_tokens, g.nc,
+                       g.ncp, counts, expert_count, expert_offset, rank_count, rank_offset, pos,
+                       row_src, bound, tickets, status, gen, flags, sync_limit_ticks());
     return hipGetLastError();
   }
   hipLaunchKernelGGL(layout_count_kernel<KW>, dim3(g.nc), dim3(kBlock), lds_count, stream,
                      idx, T, k, E, peer_L, g.chunk_tokens, g.ncp, counts, status);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((layout_place_kernel<KW, false, FIXED>), dim3(g.nc), dim3(kBlock),
-                     lds_place, stream, idx, T, k, E, peer_L, R, C, g.chunk_tokens, g.nc, g.ncp, counts,
-                     expert_count,
-                     expert_offset, rank_count, rank_offset, pos, row_src, bound, tickets,
-                     status);
+  hipLaunchKernelGGL((layout_place_kernel<KW, kPlaceAfterCount, FIXED>), dim3(g.nc),
+                     dim3(kBlock), lds_place, stream, idx, T, k, E, peer_L, R, C,
+                     g.chunk_tokens, g.nc, g.ncp, counts, expert_count, expert_offset,
+                     rank_count, rank_offset, pos, row_src, bound, tickets, status, gen, flags,
+                     (uint64_t)0);
   return hipGetLastError();
 }
 
@@ -451,9 +666,15 @@ LayoutGeom layout_geom(int64_t T, int E) {
   g.ncp = (E + 3) / 4 * 4;
   g.plan_bytes = ((size_t)(MOE_PLAN_PARTS + 1) * 4 + 255) / 256 * 256;
   g.ticket_offset = g.plan_bytes;
+  g.gen_offset = g.ticket_offset + 128;
   g.counts_offset = g.ticket_offset + 256;
   g.counts_bytes = (size_t)g.nc * g.ncp * 4;
   g.total = g.counts_offset + (g.counts_bytes + 255) / 256 * 256;
+  g.sync_offset = 0;
+  if (g.chunk_tokens == kBlock && g.nc > 1 && g.nc <= kMaxSyncChunks) {
+    g.sync_offset = g.total;
+    g.total += ((size_t)g.nc * 8 + 255) / 256 * 256;
+  }
   return g;
 }
 

@@ -28,10 +28,20 @@ struct LayoutGeom {
   int ncp;              // row pitch of the count matrix: E rounded up to 4
   size_t plan_bytes;    // bound[MOE_PLAN_PARTS + 1], padded to 256 bytes
   size_t ticket_offset; // 8 uint32 work tickets ({next, done} of dispatch, combine, expand)
+  size_t gen_offset;    // uint64 generation word of the one-launch layout (ticket block + 128)
   size_t counts_offset;
   size_t counts_bytes;  // int32 [nc][ncp], chunk-major
+  size_t sync_offset;   // uint64 arrival flags [nc] of the one-launch layout; 0: none
   size_t total;
 };
+
+// The one-launch layout (count, grid barrier, place) serves batches whose
+// chunks are single 256-token sub-chunks and whose chunk count is at most
+// this; larger grids use the count and place launches.  Each workgroup's
+// arrival costs an L2 write-back and invalidate, and those serialize: on
+// MI355X the fused form took 12.2 us against 14.3 for two launches at 16
+// chunks, tied at 64 and was slower at 128.
+constexpr int kMaxSyncChunks = 32;
 
 LayoutGeom layout_geom(int64_t T, int E);
 

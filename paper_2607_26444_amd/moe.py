@@ -28,6 +28,7 @@ MOE_DTYPE_FP8_E4M3 = 1
 MOE_STATUS_BAD_INDEX = 1
 MOE_STATUS_DUP_INDEX = 2
 MOE_STATUS_CAPACITY = 4
+MOE_STATUS_LAYOUT_SYNC = 8
 
 MOE_MAX_K = 32
 MOE_MAX_EXPERTS = 1024

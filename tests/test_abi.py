@@ -50,7 +50,7 @@ def test_binding_constants_match_the_header():
 
 
 def test_version_and_strerror():
-    assert moe.moe_version() == 4
+    assert moe.moe_version() == 5
     for code in (0, -1, -2, -3, -4, -99):
         assert isinstance(moe.lib().moe_strerror(code), bytes)
 

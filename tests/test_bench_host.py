@@ -57,3 +57,28 @@ def test_traffic_figure_is_dropped_when_the_kernel_source_changes(tmp_path, monk
     (csrc / "moe_internal.h").write_text("header changed\n")
     assert bench.read_traffic("w", "dispatch") is None
     assert bench.read_traffic("other", "dispatch") is None
+
+
+def test_read_write_split_adds_up_to_the_kernel_bytes():
+    for name in ("tiny", "decode", "prefill", "fp8", "large"):
+        b = bench.algorithmic_bytes(wl.get(name))
+        assert b["dispatch_read"] + b["dispatch_write"] == b["dispatch"]
+        assert b["combine_read"] + b["combine_write"] == b["combine"]
+        # every routed slot writes one x row; combine reads k expert rows per
+        # written y row (all slots routed in these workloads)
+        k = wl.get(name)["k"]
+        assert b["dispatch_write"] == k * (b["dispatch_read"] - 4 * b["n"])
+        assert b["combine_read"] - 8 * b["n"] == k * b["combine_write"]
+
+
+def test_stream_ceiling_is_the_time_weighted_rate():
+    # equal rates: the ceiling is that rate
+    assert bench.stream_ceiling(3e9, 5e9, 6000.0, 6000.0) == pytest.approx(6000.0)
+    # 1 GB read at 8000 GB/s (0.125 ms) + 7 GB written at 5000 GB/s (1.4 ms)
+    assert bench.stream_ceiling(1e9, 7e9, 8000.0, 5000.0) == pytest.approx(8e9 / 1.525e-3 / 1e9)
+    # pure streams give back their own rate
+    assert bench.stream_ceiling(0, 2e9, 7000.0, 5000.0) == pytest.approx(5000.0)
+    assert bench.stream_ceiling(2e9, 0, 7000.0, 5000.0) == pytest.approx(7000.0)
+    # the ceiling lies between the two rates
+    c = bench.stream_ceiling(1e9, 1e9, 7000.0, 5000.0)
+    assert 5000.0 < c < 7000.0
