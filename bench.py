@@ -129,9 +129,11 @@ def stream_ceiling(read_bytes, write_bytes, read_GBps, write_GBps):
 
 def measure_stream_legs(dev, stream, read_bytes, write_bytes, reps=10):
     """Pure-write and pure-read rates on this GPU, built from torch ops (no
-    kernel of this library): fill_ of a buffer of write_bytes, and a float32
-    sum and an int32 max over a buffer of read_bytes (the faster of the two
-    counts).  GB/s of the bytes each op moves."""
+    kernel of this library): fill_ of a buffer of write_bytes, and reductions
+    over a buffer of read_bytes -- a float32 sum along rows of 4096, a bf16
+    matrix-vector product over rows of 4096 and a whole-buffer float32 sum
+    (the fastest counts; on MI355X the row sum reads ~6.4 TB/s, the
+    whole-buffer sum ~4 TB/s).  GB/s of the bytes each op moves."""
     import torch
     out = {}
     buf = torch.empty(max(1 << 20, write_bytes // 16 * 16), dtype=torch.uint8, device=dev)
@@ -148,8 +150,11 @@ def measure_stream_legs(dev, stream, read_bytes, write_bytes, reps=10):
     del buf
     buf = torch.zeros(max(1 << 20, read_bytes // 16 * 16), dtype=torch.uint8, device=dev)
     rates = {}
-    for name, op in (("sum_f32", lambda b: b.view(torch.float32).sum()),
-                     ("max_i32", lambda b: b.view(torch.int32).amax())):
+    buf = buf[: buf.numel() // (1 << 14) * (1 << 14)]   # whole rows of 4096 float32
+    vec = torch.ones(4096, dtype=torch.bfloat16, device=dev)
+    for name, op in (("rowsum_f32", lambda b: b.view(torch.float32).view(-1, 4096).sum(dim=1)),
+                     ("mv_bf16", lambda b: torch.mv(b.view(torch.bfloat16).view(-1, 4096), vec)),
+                     ("sum_f32", lambda b: b.view(torch.float32).sum())):
         for _ in range(3):
             op(buf)
         e0.record(stream)

@@ -162,7 +162,7 @@ int moe_layout(const int32_t* topk_idx, int64_t T, int k, int E, int R,
  * forbid hipMalloc): the same kernels and the same outputs, but the
  * workspace is the library's own, a fixed device array of 576 KiB per GPU
  * (held until the process ends), large enough for every shape the library
- * accepts (moe_layout_workspace_bytes never exceeds 573952 bytes).  This
+ * accepts (moe_layout_workspace_bytes never exceeds 581888 bytes).  This
  * call allocates and frees nothing.
  *
  * In/out: as moe_layout, without the workspace arguments.
@@ -242,7 +242,7 @@ int moe_layout_fixed(const int32_t* topk_idx, int64_t T, int k, int E, int R, in
  * recv_cap  [R] int32 capacity of each region in rows.
  * topk_idx, pos, rank_offset, workspace: as produced by moe_layout.  Parts
  *           of the plan are handed out at run time from a counter in the
- *           workspace (all but each wavefront's first when parts carry 128
+ *           workspace (all but each wavefront's first when parts carry 64
  *           KiB or more, else the second half; MOE_POLICY_BALANCED of
  *           moe_dispatch_ex): two dispatch calls that share a workspace must
  *           not run at the same time on different streams.
@@ -258,13 +258,14 @@ int moe_dispatch(const void* x, const float* x_scales, int dtype, int64_t T, int
 /* Work-split policies of moe_dispatch_ex / moe_combine_ex (all give
  * bit-identical regions and identical y). */
 #define MOE_POLICY_BALANCED 0 /* byte-balanced parts, the library's choice: when a
-                               * part carries 128 KiB or more on average, every part
-                               * after each wavefront's first is handed out at run
-                               * time (dispatch and combine); smaller parts: dispatch
-                               * assigns the first half statically and hands the rest
-                               * out at run time (all statically when a wavefront
-                               * would own fewer than 8 parts), combine assigns all
-                               * statically (moe_dispatch, moe_combine) */
+                               * part carries 64 KiB (dispatch) or 128 KiB (combine)
+                               * or more on average, every part after each
+                               * wavefront's first is handed out at run time;
+                               * smaller parts: dispatch assigns the first half
+                               * statically and hands the rest out at run time (all
+                               * statically when a wavefront would own fewer than 8
+                               * parts), combine assigns all statically
+                               * (moe_dispatch, moe_combine) */
 #define MOE_POLICY_ROWS 1     /* pull: the N routed rows split evenly over wavefronts */
 #define MOE_POLICY_BY_RANK 2  /* pull: a fixed group of W/R wavefronts per rank */
 #define MOE_POLICY_DYNAMIC 3  /* push; every part after the first handed out at run time */

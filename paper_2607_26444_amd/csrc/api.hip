@@ -291,7 +291,7 @@ int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weig
   a.launch_waves = waves;
   a.rows_hint = rows_hint;
   a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
-                                          ticket_offset) + 2;
+                                          ticket_offset) + moe::kTicketGroupWords;
   return launched(moe::launch_combine(a, policy, as_stream(stream)));
 }
 
@@ -439,7 +439,8 @@ int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype,
   a.tok_offset = tok_offset;
   a.bound = static_cast<const int32_t*>(workspace);
   a.tickets = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
-                                          moe::layout_geom(T, E).ticket_offset) + 4;
+                                          moe::layout_geom(T, E).ticket_offset) +
+              2 * moe::kTicketGroupWords;
   a.status = status;
   return launched(moe::launch_expand(a, as_stream(stream)));
 }

@@ -260,7 +260,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
     }
   }
   });
-  finish_parts<DYN ? kPartsClaimed : kPartsStatic>(a.tickets, W, lane);
+  finish_parts<DYN ? kPartsClaimed : kPartsStatic>(a.tickets, g, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
   trace_wave(a.trace, a.trace_waves, g, t_start, lane);

@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
     }
   }
   });
-  finish_parts<MODE>(a.tickets, W, lane);
+  finish_parts<MODE>(a.tickets, g, W, lane);
   st = wave_or(st);
   if (st && lane == 0) atomicOr(a.status, st);
 }

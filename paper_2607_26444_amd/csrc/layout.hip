@@ -453,7 +453,9 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       rank_offset[R] = FIXED ? E * C : (int32_t)n_total;
       bound[0] = 0;
     }
-    if (tid < 8) tickets[tid] = 0u;  // work tickets of dispatch, combine, expand
+    // work tickets of dispatch, combine and expand: {next, done} of every shard
+    if (tid < kTicketGroups * 16 * 2)   // every line a group can hold
+      tickets[(tid >> 1) * kTicketStride + (tid & 1)] = 0u;
     for (int r = tid; r < R; r += kBlock) {
       rank_offset[r] = FIXED ? r * L * C : eoff[r * L];
       rank_count[r] = eoff[(r + 1) * L] - eoff[r * L];
@@ -666,8 +668,8 @@ LayoutGeom layout_geom(int64_t T, int E) {
   g.ncp = (E + 3) / 4 * 4;
   g.plan_bytes = ((size_t)(MOE_PLAN_PARTS + 1) * 4 + 255) / 256 * 256;
   g.ticket_offset = g.plan_bytes;
-  g.gen_offset = g.ticket_offset + 128;
-  g.counts_offset = g.ticket_offset + 256;
+  g.gen_offset = g.ticket_offset + kTicketBlockBytes - 128;
+  g.counts_offset = g.ticket_offset + kTicketBlockBytes;
   g.counts_bytes = (size_t)g.nc * g.ncp * 4;
   g.total = g.counts_offset + (g.counts_bytes + 255) / 256 * 256;
   g.sync_offset = 0;

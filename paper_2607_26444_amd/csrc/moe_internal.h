@@ -27,8 +27,8 @@ struct LayoutGeom {
   int nc;
   int ncp;              // row pitch of the count matrix: E rounded up to 4
   size_t plan_bytes;    // bound[MOE_PLAN_PARTS + 1], padded to 256 bytes
-  size_t ticket_offset; // 8 uint32 work tickets ({next, done} of dispatch, combine, expand)
-  size_t gen_offset;    // uint64 generation word of the one-launch layout (ticket block + 128)
+  size_t ticket_offset; // work tickets: kTicketBlockBytes (three sharded groups, see below)
+  size_t gen_offset;    // uint64 generation word of the one-launch layout (end of that block)
   size_t counts_offset;
   size_t counts_bytes;  // int32 [nc][ncp], chunk-major
   size_t sync_offset;   // uint64 arrival flags [nc] of the one-launch layout; 0: none
@@ -74,22 +74,23 @@ int copy_waves(const void* kernel, int64_t per_wave, int64_t target, int min_wav
 constexpr int64_t kDispatchInFlight = 64ll << 20;
 constexpr int64_t kCombineInFlight = 16ll << 20;
 
-// The default split (MOE_POLICY_BALANCED) hands every part out at run time
-// when a part carries at least this many algorithmic bytes on average
-// (tokens * row bytes * (1 + rows per token) / MOE_PLAN_PARTS).  Measured on
-// MI355X with a fresh x per step: claiming every part made dispatch 4-6% and
-// combine 2-4% faster at 168-192 KiB per part (prefill, large, fp8
-// combine), 1% slower at 84 KiB (fp8 dispatch) and 43-78% slower at 42 KiB
-// (decode), where one claim serves a third of a token and the claims
-// serialize on the counter.
+// The default split (MOE_POLICY_BALANCED) of combine and expand hands every
+// part out at run time when a part carries at least this many algorithmic
+// bytes on average (tokens * row bytes * (1 + rows per token) /
+// MOE_PLAN_PARTS).  Measured on MI355X with a fresh x per step: claiming
+// every part made combine 2-4% faster at 168-192 KiB per part (prefill,
+// large, fp8 combine) and, even with sharded tickets, 19% slower at 42 KiB
+// (decode: 104.5 vs 87.8 us), where one claim serves a third of a token.
 constexpr int64_t kClaimAllPartBytes = 128ll << 10;
 
-// Pair-row dispatch of the per-peer path claims every part from half that
-// size: its parts mix tokens with one to k pair rows, and claiming every
-// part measured 4% faster at 93 KiB per part (Zipf-skewed prefill) and
-// 0.6% at 107 KiB, where the same split of the source-side sum was 2-5%
+// Dispatch (per-slot rows and the per-peer path's pair rows) claims every
+// part from half that size.  With sharded tickets, claiming every part
+// measured 1.8% faster for the fp8 workload's 84 KiB parts (215 vs 219 us)
+// and tied at decode size (42 KiB, which keeps the half-claimed split);
+// pair rows measured 4% faster at 93 KiB per part (Zipf-skewed prefill)
+// and 0.6% at 107 KiB, where the same split of the source-side sum was 2-5%
 // slower and stays at the default.
-constexpr int64_t kClaimAllPairPartBytes = 64ll << 10;
+constexpr int64_t kClaimAllDispatchPartBytes = 64ll << 10;
 
 __host__ __forceinline__ bool claim_all_parts(int64_t tokens, int64_t row_bytes, int64_t rows,
                                               int64_t min_part_bytes = kClaimAllPartBytes) {
@@ -211,6 +212,49 @@ __device__ __forceinline__ float readlane_f32(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
+// Work tickets.  Each copy kernel that hands parts out at run time (dispatch,
+// combine, expand) has a group of kTicketShards counters, each {next claim,
+// wavefronts done} on its own 128-byte line; group k starts at word
+// k * kTicketGroupWords of the ticket block.  On MI355X device-scope atomics
+// on one address serialize at ~13 ns each: one counter for all wavefronts
+// capped dispatch at ~80 claims per microsecond (claiming every part at
+// decode size was bound by that alone) and made a thousand wavefronts that
+// reach their first claim together wait ~25 us.  With each shard spread over
+// all XCDs (below), 4 shards measured best of 1, 4, 8 and 16 at every
+// workload: whole steps 0.3-0.8% faster than one counter, mostly in combine.
+constexpr int kTicketShards = 4;
+constexpr int kTicketStride = 32;                                  // words (128 bytes)
+// Wavefronts are given to shards in runs of kShardSpan = 32 (eight
+// workgroups, which the hardware places on the eight XCDs in turn), so every
+// shard draws wavefronts from every XCD and the shards advance at the same
+// rate; a shard of wavefronts from one or two XCDs fell behind the others.
+constexpr int kShardSpan = 32;
+
+// Shards a launch of W wavefronts uses: one per run of kShardSpan
+// wavefronts, at most kTicketShards, so that every shard has wavefronts
+// (a shard without any would leave its claims untaken).
+__device__ __forceinline__ int ticket_shards(int W) {
+  const int n = (W + kShardSpan - 1) / kShardSpan;
+  return n < kTicketShards ? n : kTicketShards;
+}
+
+__device__ __forceinline__ int ticket_shard(int g, int W) {
+  return (g / kShardSpan) % ticket_shards(W);
+}
+
+// Number of wavefronts g < W with ticket_shard(g, W) == s.
+__device__ __forceinline__ int waves_in_shard(int s, int W) {
+  const int ns = ticket_shards(W);
+  const int runs = W / kShardSpan, rem = W % kShardSpan;
+  int n = (runs / ns + (runs % ns > s ? 1 : 0)) * kShardSpan;
+  if (rem && runs % ns == s) n += rem;
+  return n;
+}
+constexpr int kTicketGroupWords = 16 * kTicketStride;              // 2 KiB per kernel (<= 16 shards)
+constexpr int kTicketGroups = 3;                                   // dispatch, combine, expand
+constexpr size_t kTicketBlockBytes = 8192;                         // groups + generation word
+static_assert(kTicketGroups * kTicketGroupWords * 4 + 128 <= (int)kTicketBlockBytes, "tickets");
+
 // How a copy kernel's wavefronts take the parts of the plan.
 //   kPartsStatic  wavefront g of W takes parts g, g + W, g + 2W, ...
 //   kPartsClaimed wavefront g takes part g, then claims the next unclaimed
@@ -219,18 +263,23 @@ __device__ __forceinline__ float readlane_f32(float v, int l) {
 //                 claimed two at a time
 // Claimed parts come in plan order, so the wavefronts still sweep the tokens
 // as one front; claiming lets fast wavefronts take over the tail of slow
-// ones without waiting on anyone.  moe_layout zeroes the counters and the
-// last wavefront of a claiming launch resets them for the next one.
+// ones without waiting on anyone.  Wavefront g claims from shard
+// ticket_shard(g, W) of its kernel's ticket group: claim c of shard s is the
+// (c * n + s)-th claim of the plan (n = shards in use), so the shards
+// interleave in plan order and each is shared by 1/n of the wavefronts.  moe_layout zeroes the counters and the
+// last wavefront of each shard resets that shard for the next launch.
 constexpr int kPartsStatic = 0;
 constexpr int kPartsClaimed = 1;
 constexpr int kPartsHybrid = 2;
 
 template <int MODE>
-__device__ __forceinline__ void finish_parts(uint32_t* tickets, int W, int lane) {
+__device__ __forceinline__ void finish_parts(uint32_t* tickets, int g, int W, int lane) {
   if (MODE != kPartsStatic && lane == 0) {
-    if (atomicAdd(&tickets[1], 1u) == (uint32_t)(W - 1)) {
-      tickets[0] = 0u;
-      tickets[1] = 0u;
+    const int s = ticket_shard(g, W);
+    uint32_t* line = tickets + s * kTicketStride;
+    if (atomicAdd(&line[1], 1u) == (uint32_t)waves_in_shard(s, W) - 1u) {
+      line[0] = 0u;
+      line[1] = 0u;
     }
   }
 }
@@ -272,13 +321,17 @@ __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* ti
     for (int i = 0; i < n; ++i) call(b0, b1, nonempty, i);
   }
   if (MODE == kPartsStatic) return;
-  // claimed share: parts from `first` on, G per ticket
+  // claimed share: parts from `first` on, G per claim, from this
+  // wavefront's shard (claim c of shard s covers claim c * shards + s)
   constexpr int G = MODE == kPartsHybrid ? 2 : 1;
   const int first = MODE == kPartsHybrid ? S : W;
+  const int shards = ticket_shards(W);
+  const int shard = ticket_shard(g, W);
+  uint32_t* next_claim = tickets + shard * kTicketStride;
   for (;;) {
     int t = 0;
-    if (lane == 0) t = (int)atomicAdd(&tickets[0], 1u);
-    const int p0 = first + __builtin_amdgcn_readfirstlane(t) * G;
+    if (lane == 0) t = (int)atomicAdd(next_claim, 1u);
+    const int p0 = first + (__builtin_amdgcn_readfirstlane(t) * shards + shard) * G;
     if (p0 >= MOE_PLAN_PARTS) break;
     int b0 = 0, b1 = 0;
     if (lane < G && p0 + lane < MOE_PLAN_PARTS) {

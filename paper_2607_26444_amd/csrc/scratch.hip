@@ -6,7 +6,7 @@
 // matrix) is bounded for every shape the library accepts: the count matrix
 // has at most max(1, 32768 / E) rows of E rounded up to 4 int32, which is
 // largest at E = 1 (512 KiB), so the whole workspace never exceeds
-// 573952 bytes.  It lives in one file-scope device array per GPU.  Host code
+// 581888 bytes.  It lives in one file-scope device array per GPU.  Host code
 // never passes that array's name to a kernel: the name is a host-side
 // stand-in; its device address is looked up once per device with
 // hipGetSymbolAddress and kept per device.

@@ -139,16 +139,24 @@ class GpuRun:
         return regions.buf.cpu().numpy(), regions.offsets
 
 
-# The eight uint32 work tickets ({next part, wavefronts done} of dispatch,
-# combine and expand, then two spare) sit right after the plan, which is
-# bound[MOE_PLAN_PARTS + 1] padded to 256 bytes (the library's internal
-# workspace layout).
+# The work tickets sit right after the plan, which is bound[MOE_PLAN_PARTS +
+# 1] padded to 256 bytes (the library's internal workspace layout): three
+# groups (dispatch, combine, expand) of 16 shards, each shard {next claim,
+# wavefronts done} at the start of its own 128-byte line.
 TICKET_OFFSET = ((moe.MOE_PLAN_PARTS + 1) * 4 + 255) // 256 * 256
+TICKET_LINES = 3 * 16
+TICKET_BYTES = TICKET_LINES * 128
+
+
+def ticket_words(raw: np.ndarray) -> np.ndarray:
+    """{next, done} of every shard from the raw int32 ticket block."""
+    return raw[: TICKET_LINES * 32].reshape(TICKET_LINES, 32)[:, :2].ravel()
 
 
 def tickets(workspace) -> np.ndarray:
     torch.cuda.synchronize()
-    return workspace[TICKET_OFFSET: TICKET_OFFSET + 32].view(torch.int32).cpu().numpy()
+    raw = workspace[TICKET_OFFSET: TICKET_OFFSET + TICKET_BYTES].view(torch.int32).cpu().numpy()
+    return ticket_words(raw)
 
 
 def check_tickets_zero(workspace, what):

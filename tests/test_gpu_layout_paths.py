@@ -23,9 +23,10 @@ import workloads as wl  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 PLAN_PARTS = 12288
-# The generation word sits 128 bytes into the ticket block, which follows
-# the plan bound[PLAN_PARTS + 1] padded to 256 bytes (internal layout).
-GEN_OFFSET = ((PLAN_PARTS + 1) * 4 + 255) // 256 * 256 + 128
+# The generation word sits in the last 128 bytes of the 8 KiB ticket block,
+# which follows the plan bound[PLAN_PARTS + 1] padded to 256 bytes (internal
+# layout).
+GEN_OFFSET = ((PLAN_PARTS + 1) * 4 + 255) // 256 * 256 + 8192 - 128
 
 
 @pytest.fixture(scope="module", autouse=True)

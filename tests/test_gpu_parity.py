@@ -197,10 +197,21 @@ def test_dynamic_policy_matches_oracle(T, H, E, R, k, payload, mask):
 @pytest.mark.parametrize("waves", [64, 256, 3072])
 def test_explicit_wave_counts_match_oracle(policy, cpolicy, waves):
     """Every work split gives the oracle's bytes and y at a chosen wavefront
-    count, below and above what the device holds at once."""
+    count, below and above what the device holds at once (64 wavefronts use
+    two of the four ticket shards)."""
     T, H, E, R, k = 2500, 1536, 64, 16, 6
     cfg = wl.custom(T, H, E, R, k, zipf_s=1.2, seed=waves + policy)
     _full_parity(cfg, policy=policy, combine_policy=cpolicy, waves=waves, repeat=2)
+
+
+@pytest.mark.parametrize("waves", [4, 96])
+def test_claims_with_fewer_wavefronts_than_shards(waves):
+    """Claiming every part with 4 or 96 wavefronts, which fill one or three
+    runs of 32 and so use one or three ticket shards: every shard in use has
+    wavefronts, so no claim is left untaken."""
+    T, H, E, R, k = 1500, 2048, 64, 16, 8
+    cfg = wl.custom(T, H, E, R, k, zipf_s=1.2, seed=waves)
+    _full_parity(cfg, policy=3, combine_policy=3, waves=waves, repeat=2)
 
 
 @pytest.mark.parametrize("cpolicy,waves", [(0, 64), (0, 3072), (3, 256), (3, 3072)])

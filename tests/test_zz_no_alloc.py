@@ -120,7 +120,7 @@ def test_layout_scratch_matches_layout_twice():
         caps = lay.rank_count.cpu().numpy().astype(np.int32) + 1
         lay_out = dict(out)
         regions_s, y_s = _step(h, moe, cfg, inp, idx_d, w_d, x_d, lay_out, ws, caps)
-        tick = _read_device(ws.ptr + h.TICKET_OFFSET, 32).view(np.int32)
+        tick = h.ticket_words(_read_device(ws.ptr + h.TICKET_OFFSET, h.TICKET_BYTES).view(np.int32))
         assert not tick.any(), tick
         lay_ref = dict(pos=lay.pos, rank_offset=lay.rank_offset,
                        expert_offset=lay.expert_offset, status=lay.status)
