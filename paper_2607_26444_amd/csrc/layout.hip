@@ -219,28 +219,33 @@ __device__ __forceinline__ void write_plan(int32_t* __restrict__ bound, int64_t 
   constexpr int64_t P = MOE_PLAN_PARTS;
   constexpr int64_t kStride = 4 * kBlock;    // parts between a thread's groups
   const int64_t q0 = (p_first >> 2) + threadIdx.x;
-  if (q0 > (p_last >> 2)) return;
-  const int64_t qA = A / P, rA = A - qA * P;
-  const int64_t sA = kStride * A;
-  const int64_t qS = sA / P, rS = sA - qS * P;
+  const int64_t q_last = p_last >> 2;
+  if (q0 > q_last) return;
+  // Units (< A <= 2^31), remainders (< P) and the per-step increments fit
+  // 32 bits; only the first quotient needs 64-bit arithmetic.
+  const int32_t qA = (int32_t)(A / P), rA = (int32_t)(A - (A / P) * P);
+  const int32_t qS = (int32_t)(kStride * A / P), rS = (int32_t)(kStride * A - (kStride * A / P) * P);
   // (u, r): floor quotient and remainder of 4q*A - 1 by P for the group's
-  // first part p0 = 4q (p0 = 0 gives -1: u = -1, r = P - 1)
+  // first part p0 = 4q (p0 = 0 gives -1: u = -1, r = P - 1); u is kept
+  // relative to the sub-chunk's first unit
   const int64_t n0 = 4 * q0 * A - 1;
-  int64_t u = n0 >= 0 ? n0 / P : -1;
-  int64_t r = n0 - u * P;
-  for (int64_t q = q0; q <= (p_last >> 2); q += kBlock) {
+  const int64_t u0 = n0 >= 0 ? n0 / P : -1;
+  int32_t u = (int32_t)(u0 - cost_base);
+  int32_t r = (int32_t)(n0 - u0 * P);
+  const int32_t last_unit = (int32_t)n_units - 1;
+#pragma unroll 4
+  for (int64_t q = q0; q <= q_last; q += kBlock) {
     const int64_t p0 = q * 4;
     int v[4];
-    int64_t uu = u, rr = r;
+    int32_t uu = u, rr = r;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       // unconditional (clamped) lookup: the four LDS reads go out together
-      const int64_t ui = min(max(uu - cost_base, (int64_t)0), n_units - 1);
-      v[i] = (int)(s0 + owner[ui] + 1);
+      v[i] = (int)s0 + owner[min(max(uu, 0), last_unit)] + 1;
       uu += qA;
       rr += rA;
-      if (rr >= P) {
-        rr -= P;
+      if (rr >= (int32_t)P) {
+        rr -= (int32_t)P;
         ++uu;
       }
     }
@@ -253,11 +258,22 @@ __device__ __forceinline__ void write_plan(int32_t* __restrict__ bound, int64_t 
     }
     u += qS;
     r += rS;
-    if (r >= P) {
-      r -= P;
+    if (r >= (int32_t)P) {
+      r -= (int32_t)P;
       ++u;
     }
   }
+}
+
+// Sets bound[p] = v for p in [pa, pb]: scalar stores up to a 16-byte
+// boundary, then 16-byte stores, then the scalar tail.
+constexpr int64_t kFillParts = 1024;   // longest run a thread fills
+__device__ __forceinline__ void fill_plan(int32_t* __restrict__ bound, int64_t pa, int64_t pb,
+                                          int32_t v) {
+  int64_t p = pa;
+  for (; p <= pb && (p & 3); ++p) bound[p] = v;
+  for (; p + 3 <= pb; p += 4) *reinterpret_cast<int4*>(bound + p) = int4{v, v, v, v};
+  for (; p <= pb; ++p) bound[p] = v;
 }
 
 // FIXED: fixed-capacity windows of C rows per expert (expert e's window
@@ -541,21 +557,29 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
       }
     }
     // Plan boundaries inside this sub-chunk: token t owns the parts p with
-    // a_t*P < p*A <= (a_t + cost_t)*P, each starting at token t+1.  In cost
-    // units, part p starts inside unit ceil(p*A/P) - 1, so the sub-chunk's
-    // units are mapped to their tokens in LDS and the parts are written
-    // part-major, four neighbouring parts per thread (coalesced; a token may
-    // own hundreds of parts when there are few tokens).
+    // a_t*P < p*A <= (a_t + cost_t)*P, each starting at token t+1.  When no
+    // token can own more than kFillParts parts, each thread fills its own
+    // token's run (a constant; 16-byte stores inside the run).  Otherwise
+    // (batches of a few tokens, where one token may own thousands of parts)
+    // the sub-chunk's cost units are mapped to their tokens in LDS and the
+    // parts are written part-major (write_plan).  Measured on MI355X for the
+    // 128-token, one-workgroup layout: filling runs 0.5 us, part-major 2.6.
     const int64_t cost = (t < c1) ? 1 + nplaced : 0;
     uint32_t ex32, unused_e, sub32, unused_t;
     block_exclusive_scan2((uint32_t)cost, 0u, reinterpret_cast<uint32_t*>(scan), ex32, unused_e,
                           sub32, unused_t);
     const int64_t ex = ex32, sub_total = sub32;
-    for (int64_t u = ex; u < ex + cost; ++u) owner[u] = (uint16_t)tid;
-    __syncthreads();
-    const int64_t p_first = (cost_base * P) / A + 1;
-    const int64_t p_last = ((cost_base + sub_total) * P) / A;
-    write_plan(bound, p_first, p_last, A, cost_base, sub_total, owner, s0);
+    if ((int64_t)P * (1 + KW) <= kFillParts * A) {
+      if (cost > 0)
+        fill_plan(bound, ((cost_base + ex) * P) / A + 1, ((cost_base + ex + cost) * P) / A,
+                  (int32_t)(t + 1));
+    } else {
+      for (int64_t u = ex; u < ex + cost; ++u) owner[u] = (uint16_t)tid;
+      __syncthreads();
+      const int64_t p_first = (cost_base * P) / A + 1;
+      const int64_t p_last = ((cost_base + sub_total) * P) / A;
+      write_plan(bound, p_first, p_last, A, cost_base, sub_total, owner, s0);
+    }
     cost_base += sub_total;
     for (int i = tid; i < kWavesPerBlock * E; i += kBlock) mask[i] = 0;
     __syncthreads();

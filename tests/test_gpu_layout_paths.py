@@ -93,6 +93,9 @@ def _check(lay, idx, E, R, capacity=None, what=""):
     (9000, 1024, 64, 8, 0.0, 0.1),    # two launches: 512-token chunks, E = 1024
     (200, 64, 16, 4, 0.0, 0.1),       # one workgroup
     (128, 16, 4, 2, 0.0, 0.0),        # one workgroup, the tiny workload's shape
+    (1, 16, 4, 2, 0.0, 0.0),          # one token owns every part: plan written part-major
+    (5, 256, 64, 8, 0.0, 0.0),        # a few tokens: plan written part-major
+    (33, 64, 16, 8, 0.0, 0.5),        # part-major with unused slots
     (4096, 16, 4, 2, 0.0, 0.0),       # fused; cost total T*(1+k) equals the plan's parts
     (8192, 16, 4, 2, 0.0, 0.0),       # fused, 32 chunks; cost total is twice the plan's parts
 ])
