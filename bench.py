@@ -477,6 +477,8 @@ def dedup_bench(a):
     dsreg = moe.Regions(prow, spitch) if fp8 else None
     reg = moe.Regions(rows, rb)
     sreg = moe.Regions(rows, spitch) if fp8 else None
+    reg_ps = moe.Regions(rows, rb)           # the per-slot reference dispatch's own
+    sreg_ps = moe.Regions(rows, spitch) if fp8 else None
     ereg = moe.Regions(rows, 2 * H)
     preg = moe.Regions(prow, 2 * H)
     y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
@@ -499,32 +501,40 @@ def dedup_bench(a):
             preg.table, H, E, R, idx_d, dl.tok_pos, dl.tok_offset, preg.cap, y, dl.workspace,
             status),
         "dispatch": lambda: moe.moe_dispatch(
-            *xs_all[cur[0]], dtype, H, E, R, idx_d, lay.pos, lay.rank_offset, reg.table,
-            sreg.table if fp8 else None, reg.cap, lay.workspace, status, scale_pitch=spitch),
+            *xs_all[cur[0]], dtype, H, E, R, idx_d, lay.pos, lay.rank_offset, reg_ps.table,
+            sreg_ps.table if fp8 else None, reg_ps.cap, lay.workspace, status,
+            scale_pitch=spitch),
         "combine": lambda: moe.moe_combine(
             ereg.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, ereg.cap, y,
             lay.workspace, status),
     }
     ops["dispatch"]()
-    moe.moe_expert_scale(reg.table, sreg.table if fp8 else None, dtype, H, E, R,
+    moe.moe_expert_scale(reg_ps.table, sreg_ps.table if fp8 else None, dtype, H, E, R,
                          cfg["expert"] == "identity", lay.expert_offset, lay.rank_offset,
-                         reg.cap, ereg.table, sum(rows), scale_pitch=spitch)
+                         reg_ps.cap, ereg.table, sum(rows), scale_pitch=spitch)
     torch.cuda.synchronize()
     names = list(ops)
-    for i in range(a.warmup):
-        cur[0] = i % len(xs_all)
-        for n in names:
-            ops[n]()
-    torch.cuda.synchronize()
+    # Each path is timed in steps of its own, as a layer runs one of them: the
+    # per-slot dispatch stores rows of 8 KiB or less with ordinary stores,
+    # and their write-back, interleaved with the per-peer chain, made the
+    # expansion 8-13% slower at the large and fp8 workloads.
+    phases = (["layout", "layout_dedup", "dispatch_dedup", "expand", "combine_local",
+               "combine_dedup"], ["dispatch", "combine"])
     ev = {n: [(Event(), Event())
               for _ in range(a.steps)] for n in names}
-    for s_ in range(a.steps):
-        cur[0] = s_ % len(xs_all)
-        for n in names:
-            ev[n][s_][0].record(stream)
-            ops[n]()
-            ev[n][s_][1].record(stream)
-    torch.cuda.synchronize()
+    for phase in phases:
+        for i in range(a.warmup):
+            cur[0] = i % len(xs_all)
+            for n in phase:
+                ops[n]()
+        torch.cuda.synchronize()
+        for s_ in range(a.steps):
+            cur[0] = s_ % len(xs_all)
+            for n in phase:
+                ev[n][s_][0].record(stream)
+                ops[n]()
+                ev[n][s_][1].record(stream)
+        torch.cuda.synchronize()
     st = int(status.item()) | int(lay.status.item()) | int(dl.status.item())
     us = {n: float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev[n]])) * 1e3 for n in names}
     row = rb + sb                        # a row and its scales (fp8)
