@@ -39,9 +39,10 @@ struct LayoutGeom {
 // chunks are single 256-token sub-chunks and whose chunk count is at most
 // this; larger grids use the count and place launches.  Each workgroup's
 // arrival costs an L2 write-back and invalidate, and those serialize: on
-// MI355X the fused form took 12.2 us against 14.3 for two launches at 16
-// chunks, tied at 64 and was slower at 128.
-constexpr int kMaxSyncChunks = 32;
+// MI355X the fused form took 11.0 us against 14.3 for two launches at 16
+// chunks (decode size), was 0.6-0.9 us faster inside whole steps at 64
+// (prefill and fp8 sizes) and slower at 128.
+constexpr int kMaxSyncChunks = 64;
 
 LayoutGeom layout_geom(int64_t T, int E);
 

@@ -3,7 +3,7 @@ grid barrier.
 
 moe_layout runs as one workgroup (T <= 256), as one launch whose
 workgroups meet at a grid barrier (one 256-token chunk per workgroup, at
-most 32 chunks), or as a count launch followed by a place launch (larger
+most 64 chunks), or as a count launch followed by a place launch (larger
 grids).  Every form must give the oracle's layout and plan bit for bit.
 The fused form keeps a generation word in the workspace (after the work
 tickets) that every fused call advances; the tests read it to tell which
@@ -38,7 +38,7 @@ def _need_gpu():
 
 
 def _form(T, E):
-    """Launch form the library picks for (T, E) on a GPU that keeps 32
+    """Launch form the library picks for (T, E) on a GPU that keeps 64
     workgroups resident: 'single', 'fused' or 'two'."""
     nc_max = 1 if E >= 32768 else 32768 // E
     per = -(-T // (256 * nc_max))
@@ -46,7 +46,7 @@ def _form(T, E):
     nc = max(1, -(-T // chunk))
     if nc == 1 and T <= 256:
         return "single"
-    return "fused" if chunk == 256 and 1 < nc <= 32 else "two"
+    return "fused" if chunk == 256 and 1 < nc <= 64 else "two"
 
 
 def _gen(lay):
@@ -83,11 +83,12 @@ def _check(lay, idx, E, R, capacity=None, what=""):
 @pytest.mark.parametrize("T,E,R,k,zipf,mask", [
     (257, 256, 64, 8, 0.0, 0.0),      # fused, 2 chunks
     (4096, 256, 64, 8, 0.0, 0.0),     # fused, decode-sized (16 chunks)
-    (8192, 256, 64, 8, 1.2, 0.0),     # fused, 32 chunks (the most), Zipf
+    (8192, 256, 64, 8, 1.2, 0.0),     # fused, 32 chunks, Zipf
+    (16384, 256, 64, 8, 1.2, 0.0),    # fused, 64 chunks (the most), Zipf
     (3000, 1, 1, 1, 0.0, 0.0),        # fused, one expert
     (5000, 1024, 64, 32, 0.0, 0.5),   # fused, widest slots and most experts
-    (8193, 256, 64, 8, 0.0, 0.1),     # two launches: 33 chunks
-    (16384, 256, 64, 8, 1.2, 0.0),    # two launches: 64 chunks, Zipf
+    (16385, 256, 64, 8, 0.0, 0.1),    # two launches: 65 chunks
+    (32768, 256, 64, 8, 0.0, 0.0),    # two launches: 128 chunks
     (65536, 16, 4, 2, 1.2, 0.0),      # two launches: 256 chunks
     (40000, 256, 64, 8, 1.2, 0.0),    # two launches: 512-token chunks
     (9000, 1024, 64, 8, 0.0, 0.1),    # two launches: 512-token chunks, E = 1024
