@@ -141,7 +141,7 @@ int moe_layout_workspace_bytes(int64_t T, int k, int E, int R, size_t* out_bytes
  *      workspace            partition plan (see above) + scratch;
  *      status               OR-ed bits (BAD_INDEX, DUP_INDEX, LAYOUT_SYNC).
  * Launches: one workgroup when T <= 256; one launch whose workgroups (one
- * per 256-token chunk, at most 64) meet at a grid barrier when the batch
+ * per 256-token chunk, at most 128) meet at a grid barrier when the batch
  * fits that; a counting launch and a placing launch otherwise.  The barrier
  * needs no cleared memory: the workspace holds a generation word that each
  * such call advances on the device, and a workgroup's arrival flag carries a

@@ -51,11 +51,7 @@ __device__ __forceinline__ void gather(u32x4 (&v)[KW], const uint8_t* const (&sr
   for (int j = 0; j < KW; ++j) v[j] = ld16_stream(src[j] + off);
 }
 
-// Buffer resources (base, range in bytes): a load at an offset outside the
-// range returns zeros and reads nothing.  Word 3 selects 32-bit untyped data
-// on gfx9-family GPUs; cache policy 2 is the non-temporal hint.
-typedef __amdgpu_buffer_rsrc_t Rsrc;
-constexpr int kRsrcWord3 = 0x00020000;
+// Buffer-resource loads (Rsrc) with cache policy 2, the non-temporal hint.
 constexpr int kLoadNonTemporal = 2;
 
 template <int KW>

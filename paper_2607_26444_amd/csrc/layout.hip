@@ -185,6 +185,21 @@ constexpr int kPlaceAfterCount = 0;
 constexpr int kPlaceSingle = 1;
 constexpr int kPlaceFused = 2;
 
+// The one-launch layout (count, grid barrier, place) serves batches whose
+// chunks are single 256-token sub-chunks and whose chunk count is at most
+// this; larger grids use the count and place launches.  On MI355X the one
+// launch took 11.0 us against 14.3 for two at 16 chunks (decode size) and
+// 12.4 against 12.9 at 128 (32768 tokens, 128 experts); at 256 chunks the
+// two forms tie.
+constexpr int kMaxSyncChunks = 128;
+
+// s_waitcnt operand that waits for every outstanding vector memory operation
+// (vmcnt 0) and leaves the other counters free (gfx9 encoding: expcnt 7 in
+// bits 6:4, lgkmcnt 15 in bits 11:8, both vmcnt fields 0).
+constexpr int kWaitVmcnt0 = 0x0F70;
+// Cache policy of a buffer load: sc1, coherent at device (agent) scope.
+constexpr int kCoherent = 16;
+
 // Grid barrier of the fused layout without a counter in a known state: the
 // workspace holds a generation word and one arrival flag per chunk.  Every
 // workgroup reads the generation g at entry and publishes its count row
@@ -196,6 +211,17 @@ constexpr int kPlaceFused = 2;
 // a workspace matches only by a 2^-64 coincidence.  Every call advances the
 // word on the device, so a call replayed from a captured graph gets a fresh
 // value as well.
+//
+// Count rows, flags and the generation word are accessed only with
+// device-coherent (agent-scope) loads and stores, which on gfx950 bypass the
+// compute unit's cache and keep the XCDs' L2 caches coherent for those
+// lines.  A workgroup waits until its count-row stores have completed
+// before it stores its flag, so a reader that sees the flag and then reads
+// the rows with coherent loads sees them complete.  No cache-wide
+// write-back or invalidate is needed: on MI355X dropping the release and
+// acquire fences (an L2 write-back and an L2 invalidate per workgroup) cut
+// the 64-chunk layout from 12.4 to 12.0 us and the 128-chunk one from 12.9
+// to 12.4.
 __device__ __forceinline__ uint64_t sync_epoch(uint64_t g) {
   uint64_t z = g + 0x9E3779B97F4A7C15ull;
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -328,11 +354,8 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     __syncthreads();
   }
   if constexpr (MODE == kPlaceFused) {
-    // Publish this chunk's count row, then wait for every chunk's.
-    // Wave 0 alone writes the row and synchronizes, so one cache write-back
-    // (release) and one invalidate (acquire) per workgroup suffice: on
-    // MI355X each costs a serialized L2 operation, and with one per wave the
-    // barrier took twice as long.
+    // Publish this chunk's count row, then wait for every chunk's (wave 0
+    // alone: one flag per workgroup).
     if (w == 0) {
       const uint64_t epoch =
           sync_epoch(__hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
@@ -340,10 +363,16 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
         int cnt = 0;
 #pragma unroll
         for (int q = 0; q < kWavesPerBlock; ++q) cnt += __popcll(mask[q * E + e]);
-        counts[(int64_t)c * ncp + e] = cnt;
+        __hip_atomic_store(counts + (int64_t)c * ncp + e, cnt, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
       }
+      // The row's stores complete (vmcnt(0)) before the flag is stored; the
+      // signal fences keep the compiler from moving either store across.
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
       if (lane == 0)
-        __hip_atomic_store(flags + c, epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(flags + c, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const uint64_t t_begin = (uint64_t)wall_clock64();
       for (;;) {
         bool here = true;   // all flags this lane checks (loads issued together)
@@ -361,14 +390,12 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
         }
         __builtin_amdgcn_s_sleep(1);
       }
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       // every workgroup read the generation before it published its flag
       if (c == 0 && lane == 0)
         __hip_atomic_store(gen, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    // The other waves read the count matrix after this barrier, ordered
-    // behind wave 0's acquire (which also invalidated this compute unit's
-    // caches).
+    // Every wave reads the count matrix after this point, with coherent
+    // loads (below).
     __syncthreads();
   }
   if (SINGLE) {
@@ -388,6 +415,9 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     const int q4 = ncp / 4;
     const int groups = min(kBlock / q4, kMaxCountGroups);
     const int gi = tid / q4, li = tid - gi * q4;
+    // fused: the rows other workgroups published in this launch, read with
+    // device-coherent 16-byte loads through a buffer resource
+    const Rsrc rows = __builtin_amdgcn_make_buffer_rsrc(counts, 0, nc * ncp * 4, kRsrcWord3);
     int32_t* part_t = woff;                   // [groups][ncp], free until placement
     int32_t* part_p = woff + groups * ncp;
     if (gi < groups) {
@@ -397,7 +427,13 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
 #pragma unroll
         for (int u = 0; u < kCountBatch; ++u) {
           const int r = min(r0 + u * groups, nc - 1);  // past nc: re-read, ignored
-          v[u] = reinterpret_cast<const int4*>(counts + (int64_t)r * ncp)[li];
+          if constexpr (MODE == kPlaceFused) {
+            const u32x4 q = __builtin_amdgcn_raw_buffer_load_b128(rows, (r * ncp + li * 4) * 4,
+                                                                  0, kCoherent);
+            v[u] = int4{(int)q.x, (int)q.y, (int)q.z, (int)q.w};
+          } else {
+            v[u] = reinterpret_cast<const int4*>(counts + (int64_t)r * ncp)[li];
+          }
         }
         __builtin_amdgcn_sched_barrier(0);  // keep every load ahead of the first use
 #pragma unroll

@@ -35,15 +35,6 @@ struct LayoutGeom {
   size_t total;
 };
 
-// The one-launch layout (count, grid barrier, place) serves batches whose
-// chunks are single 256-token sub-chunks and whose chunk count is at most
-// this; larger grids use the count and place launches.  Each workgroup's
-// arrival costs an L2 write-back and invalidate, and those serialize: on
-// MI355X the fused form took 11.0 us against 14.3 for two launches at 16
-// chunks (decode size), was 0.6-0.9 us faster inside whole steps at 64
-// (prefill and fp8 sizes) and slower at 128.
-constexpr int kMaxSyncChunks = 64;
-
 LayoutGeom layout_geom(int64_t T, int E);
 
 // MOE_OK for hipSuccess; otherwise records the error for
@@ -198,6 +189,12 @@ __device__ __forceinline__ void st16_stream(void* p, u32x4 v) {
 }
 __device__ __forceinline__ uint32_t ld4(const void* p) { return *(const gu32*)(uintptr_t)p; }
 __device__ __forceinline__ void st4(void* p, uint32_t v) { *(gu32*)(uintptr_t)p = v; }
+
+// Buffer resources (base, range in bytes): a load at an offset outside the
+// range returns zeros and reads nothing.  Word 3 selects 32-bit untyped data
+// on gfx9-family GPUs.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;
 
 // Wavefront-uniform value held in a scalar register.
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }

@@ -3,7 +3,7 @@ grid barrier.
 
 moe_layout runs as one workgroup (T <= 256), as one launch whose
 workgroups meet at a grid barrier (one 256-token chunk per workgroup, at
-most 64 chunks), or as a count launch followed by a place launch (larger
+most 128 chunks), or as a count launch followed by a place launch (larger
 grids).  Every form must give the oracle's layout and plan bit for bit.
 The fused form keeps a generation word in the workspace (after the work
 tickets) that every fused call advances; the tests read it to tell which
@@ -38,7 +38,7 @@ def _need_gpu():
 
 
 def _form(T, E):
-    """Launch form the library picks for (T, E) on a GPU that keeps 64
+    """Launch form the library picks for (T, E) on a GPU that keeps 128
     workgroups resident: 'single', 'fused' or 'two'."""
     nc_max = 1 if E >= 32768 else 32768 // E
     per = -(-T // (256 * nc_max))
@@ -46,7 +46,7 @@ def _form(T, E):
     nc = max(1, -(-T // chunk))
     if nc == 1 and T <= 256:
         return "single"
-    return "fused" if chunk == 256 and 1 < nc <= 64 else "two"
+    return "fused" if chunk == 256 and 1 < nc <= 128 else "two"
 
 
 def _gen(lay):
@@ -84,11 +84,13 @@ def _check(lay, idx, E, R, capacity=None, what=""):
     (257, 256, 64, 8, 0.0, 0.0),      # fused, 2 chunks
     (4096, 256, 64, 8, 0.0, 0.0),     # fused, decode-sized (16 chunks)
     (8192, 256, 64, 8, 1.2, 0.0),     # fused, 32 chunks, Zipf
-    (16384, 256, 64, 8, 1.2, 0.0),    # fused, 64 chunks (the most), Zipf
+    (16384, 256, 64, 8, 1.2, 0.0),    # fused, 64 chunks, Zipf
+    (16385, 256, 64, 8, 0.0, 0.1),    # fused, 65 chunks (the last one a single token)
+    (32768, 256, 64, 8, 0.0, 0.0),    # fused, 128 chunks (the most)
+    (32768, 128, 32, 8, 1.5, 0.0),    # fused, 128 chunks, E = 128, Zipf
     (3000, 1, 1, 1, 0.0, 0.0),        # fused, one expert
     (5000, 1024, 64, 32, 0.0, 0.5),   # fused, widest slots and most experts
-    (16385, 256, 64, 8, 0.0, 0.1),    # two launches: 65 chunks
-    (32768, 256, 64, 8, 0.0, 0.0),    # two launches: 128 chunks
+    (33024, 128, 32, 8, 0.0, 0.1),    # two launches: 129 chunks
     (65536, 16, 4, 2, 1.2, 0.0),      # two launches: 256 chunks
     (40000, 256, 64, 8, 1.2, 0.0),    # two launches: 512-token chunks
     (9000, 1024, 64, 8, 0.0, 0.1),    # two launches: 512-token chunks, E = 1024
@@ -122,13 +124,15 @@ def test_fixed_capacity_forms_match_oracle(T, E, R, k, C):
     _check(lay, idx, E, R, capacity=C, what=f"fixed T={T} C={C}")
 
 
+@pytest.mark.parametrize("T", [8192, 32768])
 @pytest.mark.parametrize("fill", ["zeros", "ones", "arange", "other_batch"])
-def test_fused_barrier_with_leftover_workspace(fill):
+def test_fused_barrier_with_leftover_workspace(fill, T):
     """A workspace holding leftovers must not let the barrier pass before
     every chunk has published: a count row read too early would come from
-    the leftovers (or an earlier batch) and misplace rows."""
+    the leftovers (or an earlier batch) and misplace rows.  32 and 128
+    workgroups (the most the one-launch form takes)."""
     from paper_2607_26444_amd import moe
-    T, E, R, k = 8192, 256, 64, 8
+    E, R, k = 256, 64, 8
     assert _form(T, E) == "fused"
     a = _routing(T, k, E, seed=1, zipf=1.2)
     b = _routing(T, k, E, seed=2)
