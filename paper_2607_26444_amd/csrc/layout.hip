@@ -1,8 +1,11 @@
 // Token placement and partition plan (paper Appendix D, first to third
 // level; Section 6.2 for the byte-balanced split).
 //
-// Two kernels, both one workgroup per chunk of tokens (a batch of at most
-// 256 tokens needs only the second, which then counts for itself):
+// Two kernels, both one workgroup per chunk of tokens.  A batch of at most
+// 256 tokens needs only the second, which then counts for itself; a batch
+// of at most kMaxSyncChunks chunks of 256 tokens also runs only the second,
+// whose workgroups count their chunks, exchange the counts through the
+// workspace and meet at a grid barrier before placing (kPlaceFused):
 //
 //   layout_count  per-chunk expert histogram.  Each wavefront owns 64
 //                 consecutive tokens (one per lane) and sets, for every
@@ -658,13 +661,21 @@ int resident_blocks(const void* kernel, size_t lds_bytes) {
   return cache[key] = cus * blocks;
 }
 
-// Time limit of the fused layout's grid barrier in wall-clock ticks (2 s).
+// Time limit of the fused layout's grid barrier in wall-clock ticks (2 s),
+// from the current device's wall-clock rate (queried once per device).
 uint64_t sync_limit_ticks() {
-  int dev = 0, khz = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz < 1)
+  static std::mutex mu;
+  static std::map<int, uint64_t> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(dev);
+  if (it != cache.end()) return it->second;
+  int khz = 0;
+  if (dev < 0 || hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+      khz < 1)
     khz = 100000;
-  return (uint64_t)khz * 2000u;
+  return cache[dev] = (uint64_t)khz * 2000u;
 }
 
 template <int KW, bool FIXED>
