@@ -200,3 +200,19 @@ def test_fused_layout_replayed_from_a_graph_with_new_routing():
         gen = _gen(lay)
         assert gen not in seen, i
         seen.add(gen)
+
+
+@pytest.mark.parametrize("T,E,R,k", [(4096, 256, 64, 8), (200, 64, 16, 4), (3000, 64, 16, 16)])
+def test_layout_with_index_rows_off_16_byte_alignment(T, E, R, k):
+    """Indices that start 4 bytes past a 16-byte boundary: the layout reads
+    them one slot at a time instead of as 16-byte rows, with the same
+    result."""
+    from paper_2607_26444_amd import moe
+    idx = _routing(T, k, E, seed=T + k, zipf=1.2)
+    buf = torch.zeros(T * k + 4, dtype=torch.int32, device="cuda")
+    view = buf[1:1 + T * k].view(T, k)
+    assert view.data_ptr() % 16 == 4
+    view.copy_(torch.from_numpy(idx).cuda())
+    lay = moe.Layout(T, k, E, R)
+    lay.run(view)
+    _check(lay, idx, E, R, what=f"offset T={T} k={k}")
