@@ -273,6 +273,7 @@ int combine_common(const uint64_t* expert_y, const float* topk_w, bool unit_weig
   if (!aligned(workspace, 256) || workspace_bytes < need_bytes) return MOE_EWORKSPACE;
   if (T == 0) return MOE_OK;
   moe::CombineArgs a;
+  a.R = R;
   a.expert_y = expert_y;
   a.topk_w = unit_weights ? nullptr : topk_w;
   a.tokens = T;

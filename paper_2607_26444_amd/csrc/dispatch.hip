@@ -57,10 +57,26 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
   // zeros so a token can read k entries without a bounds test.
   __shared__ uint64_t s_dst[kWavesPerBlock][kWave + MOE_MAX_K];
   __shared__ uint64_t s_sdst[kWavesPerBlock][SCALES ? kWave + MOE_MAX_K : 1];
+  // Per-rank tables (first global row, capacity, region bases), staged once
+  // per workgroup: a slot's destination is then an LDS lookup behind its pos
+  // and expert loads rather than a second, dependent global load.  Measured
+  // on MI355X in whole steps: fp8 dispatch 208.0 -> 206.8 us, large 443.9 ->
+  // 443.2, prefill and decode unchanged.
+  __shared__ int32_t s_roff[MOE_MAX_EXPERTS];
+  __shared__ int32_t s_cap[MOE_MAX_EXPERTS];
+  __shared__ uint64_t s_rx[MOE_MAX_EXPERTS];
+  __shared__ uint64_t s_rs[SCALES ? MOE_MAX_EXPERTS : 1];
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
   const int g = uniform(blockIdx.x * kWavesPerBlock + wv);
   const uint64_t t_start = a.trace ? (uint64_t)wall_clock64() : 0;
+  for (int i = threadIdx.x; i < a.R; i += kBlock) {
+    s_roff[i] = a.rank_offset[i];
+    s_cap[i] = a.recv_cap[i];
+    s_rx[i] = a.recv_x[i];
+    if (SCALES) s_rs[i] = a.recv_scales[i];
+  }
+  __syncthreads();
   const int W = gridDim.x * kWavesPerBlock;
   const uint32_t rb = (uint32_t)a.row_bytes;
   const uint32_t sb = (uint32_t)a.scale_row_bytes;
@@ -103,10 +119,10 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
       const int p = a.pos[s];
       if (p >= 0) {
         const int r = a.topk_idx[s] / a.L;
-        const int local = p - a.rank_offset[r];
-        if (local >= 0 && local < a.recv_cap[r]) {
-          dst = a.recv_x[r] + (uint64_t)local * rb;
-          if (SCALES) sdst = a.recv_scales[r] + (uint64_t)local * sp;
+        const int local = p - s_roff[r];
+        if (local >= 0 && local < s_cap[r]) {
+          dst = s_rx[r] + (uint64_t)local * rb;
+          if (SCALES) sdst = s_rs[r] + (uint64_t)local * sp;
         } else {
           st |= MOE_STATUS_CAPACITY;
         }

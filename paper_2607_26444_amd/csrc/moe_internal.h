@@ -145,6 +145,7 @@ struct CombineArgs {
   uint64_t* trace;
   int32_t trace_waves;
   uint32_t* tickets;           // dynamic policy: {next, done}, zeroed by the layout
+  int32_t R;                   // ranks (entries of expert_y, rank_offset, recv_cap)
 };
 
 hipError_t launch_combine(const CombineArgs& a, int policy, hipStream_t stream);
