@@ -111,6 +111,7 @@ def test_tiny_identity_softmax_returns_x():
     (131072, 128, 256, 64, 8, wl.BF16, 0.0),   # 1M slots, 128 layout chunks
     (90, 8192, 64, 16, 6, wl.FP8_E4M3, 0.1),   # 256-byte scale rows, k=6
     (64, 1152, 1024, 256, 8, wl.BF16, 0.0),    # maximum expert count
+    (96, 1152, 1024, 1024, 8, wl.BF16, 0.1),   # one expert per rank at the maximum: full rank tables
 ])
 def test_custom_shapes(T, H, E, R, k, payload, mask):
     cfg = wl.custom(T, H, E, R, k, payload=payload, seed=T + H)
@@ -181,6 +182,7 @@ def test_pull_policies_match_oracle(policy, T, H, E, R, k, payload, mask):
     (700, 640, 32, 8, 5, wl.FP8_E4M3, 0.05),
     (3000, 7168, 256, 64, 8, wl.BF16, 0.0),
     (100, 256, 16, 4, 2, wl.BF16, 0.0),
+    (300, 1152, 1024, 1024, 8, wl.FP8_E4M3, 0.1),   # claimed parts with 1024 rank-table entries
 ])
 def test_dynamic_policy_matches_oracle(T, H, E, R, k, payload, mask):
     """Parts handed out at run time: same bytes for dispatch, same y for
