@@ -31,6 +31,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+# Per-phase timing events go on every EVENT_EVERY-th timed step (see main).
+EVENT_EVERY = 4
+
+
+def sampled_steps(steps: int, every: int) -> list:
+    """Timed steps that carry per-phase events: 0, every, 2*every, ..."""
+    return list(range(0, steps, max(1, every)))
 
 
 def _num(v, nd):
@@ -606,6 +613,9 @@ def main(argv=None):
                     help="instead of the step benchmark: the per-peer deduplicated path")
     ap.add_argument("--graph", action="store_true",
                     help="capture each step in a graph (needs --ll: no host sync in a step)")
+    ap.add_argument("--event-every", type=int, default=EVENT_EVERY, metavar="N",
+                    help="record the per-phase timing events on every N-th timed step "
+                         "(1: every step)")
     a = ap.parse_args(argv)
     if a.steps is None:
         a.steps = 1000 if a.workload in ("tiny", "tiny_t128_h256_e16_r4_k2") else 100
@@ -694,11 +704,16 @@ def main(argv=None):
                   f"--ll {need:.2f} or more", file=sys.stderr)
         return 1
 
-    # One event per phase boundary: the event that closes a step's combine
-    # also opens the next step's layout, so a step records three events (one
-    # around a graph replay).
+    # Per-phase events on every N-th timed step (`sampled`), one per phase
+    # boundary; on consecutive sampled steps the event that closes a step's
+    # combine also opens the next step's layout.  Around a graph replay: one
+    # interval per sampled step.
+    every = max(1, a.event_every)
+    sampled = sampled_steps(a.steps, every)
     per = 1 if a.graph else 3
-    ev = [Event() for _ in range(per * a.steps + 1)]
+    ev = {}
+    for s in sampled:
+        ev[s] = [ev[s - 1][-1] if s - 1 in ev else Event()] + [Event() for _ in range(per)]
     graph = None
     if a.graph:
         # one graph per step and x copy; events stay outside it (recorded
@@ -721,20 +736,26 @@ def main(argv=None):
     print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev[0].record(stream)
     for s in range(a.steps):
         cur[0] = s % n_x
-        e = ev[per * s:per * s + per + 1]
+        e = ev.get(s)
+        if e is not None and s - 1 not in ev:
+            e[0].record(stream)
         if graph is not None:
             graph[cur[0]].replay()
-            e[1].record(stream)
-        else:
+            if e is not None:
+                e[1].record(stream)
+        elif e is not None:
             lay.run(idx_d)
             e[1].record(stream)
             dispatch()
             e[2].record(stream)
             combine()
             e[3].record(stream)
+        else:
+            lay.run(idx_d)
+            dispatch()
+            combine()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     status = int(lay.status.item())
@@ -742,13 +763,14 @@ def main(argv=None):
         print(f"[bench] status word {status} after timing", file=sys.stderr)
         return 1
 
-    # (with a graph, lay_ms holds the whole replay)
-    lay_ms = np.array([ev[per * s].elapsed_time(ev[per * s + 1]) for s in range(a.steps)])
+    # per-phase times of the sampled steps (with a graph, lay_ms holds the
+    # whole replay)
+    lay_ms = np.array([ev[s][0].elapsed_time(ev[s][1]) for s in sampled])
     if graph is not None:
-        dis_ms = com_ms = np.full(a.steps, float("nan"))
+        dis_ms = com_ms = np.full(len(sampled), float("nan"))
     else:
-        dis_ms = np.array([ev[3 * s + 1].elapsed_time(ev[3 * s + 2]) for s in range(a.steps)])
-        com_ms = np.array([ev[3 * s + 2].elapsed_time(ev[3 * s + 3]) for s in range(a.steps)])
+        dis_ms = np.array([ev[s][1].elapsed_time(ev[s][2]) for s in sampled])
+        com_ms = np.array([ev[s][2].elapsed_time(ev[s][3]) for s in sampled])
     step_ms = wall * 1e3 / a.steps
     b = algorithmic_bytes(cfg)
     dc_bytes = b["dispatch"] + b["combine"]
@@ -791,6 +813,7 @@ def main(argv=None):
         "layout_us": _num(l_us, 2),
         "dispatch_us": _num(d_us, 2),
         "combine_us": _num(c_us, 2),
+        "phase_events": {"every": every, "steps_timed": len(sampled)},
         "dispatch_GBps": _num(d_gbps, 1),
         "combine_GBps": _num(c_gbps, 1),
         "dispatch_plus_combine_GBps": _num(dc_bytes / ((d_us + c_us) * 1e-6) / 1e9, 1),

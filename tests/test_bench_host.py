@@ -82,3 +82,12 @@ def test_stream_ceiling_is_the_time_weighted_rate():
     # the ceiling lies between the two rates
     c = bench.stream_ceiling(1e9, 1e9, 7000.0, 5000.0)
     assert 5000.0 < c < 7000.0
+
+
+def test_sampled_steps():
+    """Per-phase events: every N-th timed step from the first."""
+    assert bench.sampled_steps(100, 4) == list(range(0, 100, 4))
+    assert len(bench.sampled_steps(100, bench.EVENT_EVERY)) == 25
+    assert bench.sampled_steps(5, 1) == [0, 1, 2, 3, 4]
+    assert bench.sampled_steps(5, 0) == [0, 1, 2, 3, 4]
+    assert bench.sampled_steps(3, 10) == [0]
