@@ -4,8 +4,9 @@ Under the default split, dispatch and combine hand parts out at run time
 from ticket counters in the caller's workspace, so one workspace must not
 serve two calls that run at the same time.  Separate workspaces are
 independent: two batches, each with its own layout, regions and output,
-launched back to back on two streams (dispatch, expert and combine of both
-in flight together) must each match the oracle.
+launched back to back on two streams (layout, dispatch, expert and combine
+of both in flight together; both layouts take the one-launch form with its
+grid barrier) must each match the oracle.
 """
 import numpy as np
 import pytest
@@ -48,6 +49,9 @@ class _Batch:
         self.y = torch.full((T, H), 0x5A5A, dtype=torch.int16, device="cuda")
         torch.cuda.synchronize()
 
+    def layout(self, moe):
+        self.lay.run(self.idx_d, self.stream)
+
     def dispatch(self, moe):
         c = self.cfg
         moe.moe_dispatch(self.x_d, None, moe.MOE_DTYPE_BF16, c["H"], c["E"], c["R"],
@@ -85,7 +89,9 @@ def test_two_streams_two_workspaces_match_oracle():
             bt.regions.buf.fill_(h.SENTINEL)
             bt.y.fill_(0x5A5A)
         torch.cuda.synchronize()
-        for op in ("dispatch", "expert", "combine"):
+        # both layouts run as one launch with a grid barrier (48 and 16
+        # chunks), at the same time, each on its own workspace
+        for op in ("layout", "dispatch", "expert", "combine"):
             for bt in (a, b):
                 getattr(bt, op)(moe)
         torch.cuda.synchronize()
