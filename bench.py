@@ -612,7 +612,8 @@ def main(argv=None):
     ap.add_argument("--dedup", action="store_true",
                     help="instead of the step benchmark: the per-peer deduplicated path")
     ap.add_argument("--graph", action="store_true",
-                    help="capture each step in a graph (needs --ll: no host sync in a step)")
+                    help="capture the steps in graphs, one step per x copy in each "
+                         "(needs --ll: no host sync in a step)")
     ap.add_argument("--event-every", type=int, default=EVENT_EVERY, metavar="N",
                     help="record the per-phase timing events on every N-th timed step "
                          "(1: every step)")
@@ -706,46 +707,53 @@ def main(argv=None):
 
     # Per-phase events on every N-th timed step (`sampled`), one per phase
     # boundary; on consecutive sampled steps the event that closes a step's
-    # combine also opens the next step's layout.  Around a graph replay: one
-    # interval per sampled step.
+    # combine also opens the next step's layout.
     every = max(1, a.event_every)
     sampled = sampled_steps(a.steps, every)
-    per = 1 if a.graph else 3
     ev = {}
     for s in sampled:
-        ev[s] = [ev[s - 1][-1] if s - 1 in ev else Event()] + [Event() for _ in range(per)]
+        ev[s] = [ev[s - 1][-1] if s - 1 in ev else Event()] + [Event() for _ in range(3)]
     graph = None
     if a.graph:
-        # one graph per step and x copy; events stay outside it (recorded
-        # around replays)
-        graph = []
-        for i in range(n_x):
-            cur[0] = i
+        # Graphs of consecutive steps, one step per x copy in order (the last
+        # replay may hold fewer): a replay's own start and end are paid once
+        # per graph, not once per step.  Events stay outside the graphs,
+        # around every replay.
+        def capture(n):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
-                lay.run(idx_d)
-                dispatch()
-                combine()
-            graph.append(g)
+                for i in range(n):
+                    cur[0] = i
+                    lay.run(idx_d)
+                    dispatch()
+                    combine()
+            return g
+        gsteps = n_x
+        graph = {gsteps: capture(gsteps)}
+        if a.steps % gsteps:
+            graph[a.steps % gsteps] = capture(a.steps % gsteps)
         torch.cuda.synchronize()
         for _ in range(3):
-            for g in graph:
+            for g in graph.values():
                 g.replay()
         torch.cuda.synchronize()
         stream = torch.cuda.current_stream()
+        replays = [min(gsteps, a.steps - s) for s in range(0, a.steps, gsteps)]
+        rev = [(Event(), Event()) for _ in replays]
     print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(a.steps):
+    if graph is not None:
+        for n, (e0, e1) in zip(replays, rev):
+            e0.record(stream)
+            graph[n].replay()
+            e1.record(stream)
+    for s in range(a.steps if graph is None else 0):
         cur[0] = s % n_x
         e = ev.get(s)
         if e is not None and s - 1 not in ev:
             e[0].record(stream)
-        if graph is not None:
-            graph[cur[0]].replay()
-            if e is not None:
-                e[1].record(stream)
-        elif e is not None:
+        if e is not None:
             lay.run(idx_d)
             e[1].record(stream)
             dispatch()
@@ -763,12 +771,14 @@ def main(argv=None):
         print(f"[bench] status word {status} after timing", file=sys.stderr)
         return 1
 
-    # per-phase times of the sampled steps (with a graph, lay_ms holds the
-    # whole replay)
-    lay_ms = np.array([ev[s][0].elapsed_time(ev[s][1]) for s in sampled])
+    # per-phase times of the sampled steps (with graphs, lay_ms holds each
+    # replay's time per step)
     if graph is not None:
-        dis_ms = com_ms = np.full(len(sampled), float("nan"))
+        sampled = list(range(0, a.steps, gsteps))
+        lay_ms = np.array([e0.elapsed_time(e1) / n for n, (e0, e1) in zip(replays, rev)])
+        dis_ms = com_ms = np.full(len(replays), float("nan"))
     else:
+        lay_ms = np.array([ev[s][0].elapsed_time(ev[s][1]) for s in sampled])
         dis_ms = np.array([ev[s][1].elapsed_time(ev[s][2]) for s in sampled])
         com_ms = np.array([ev[s][2].elapsed_time(ev[s][3]) for s in sampled])
     step_ms = wall * 1e3 / a.steps
@@ -778,7 +788,7 @@ def main(argv=None):
     d_us, c_us, l_us = dis_ms.mean() * 1e3, com_ms.mean() * 1e3, lay_ms.mean() * 1e3
     if graph is not None:
         # a replayed graph has no per-kernel events: whole-step figures only
-        # (lay_ms times each replay)
+        # (lay_ms: each replay's time per step)
         dom, dom_bytes, dom_us = "layout+dispatch+combine (graph)", dc_bytes, l_us
         d_us = c_us = l_us = float("nan")
         traffic = None
@@ -813,7 +823,8 @@ def main(argv=None):
         "layout_us": _num(l_us, 2),
         "dispatch_us": _num(d_us, 2),
         "combine_us": _num(c_us, 2),
-        "phase_events": {"every": every, "steps_timed": len(sampled)},
+        "phase_events": ({"every": every, "steps_timed": len(sampled)} if graph is None
+                         else {"graph_steps": gsteps, "replays": len(replays)}),
         "dispatch_GBps": _num(d_gbps, 1),
         "combine_GBps": _num(c_gbps, 1),
         "dispatch_plus_combine_GBps": _num(dc_bytes / ((d_us + c_us) * 1e-6) / 1e9, 1),
