@@ -154,11 +154,11 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
 #pragma unroll
           for (int c = 0; c < VPL; ++c) {
             const uint32_t off = seg + c * kWaveBytes + l16;
-            if (FULL || off < rb) st16_stream(dj + off, v[c]);
+            if (FULL || off < rb) store_row16<VPL>(dj + off, v[c]);
           }
           if (s16 && seg == 0) {
             uint8_t* sd = reinterpret_cast<uint8_t*>(readlane64(s_sdst[wv][l0 + j], 0));
-            if (l16 < sp) st16_stream(sd + l16, sv);
+            if (l16 < sp) store_row16<VPL>(sd + l16, sv);
           }
         }
       }

@@ -35,19 +35,6 @@
 namespace moe {
 namespace {
 
-// Row stores: non-temporal for rows of more than 8 KiB, ordinary for
-// narrower rows.  Measured in whole steps on MI355X: non-temporal stores are
-// 8-12% faster for the 14 KiB rows (prefill, decode), ordinary stores 4%
-// faster for the fp8 workload's 7 KiB rows (211 vs 220 us) and 2.5% for the
-// 8 KiB rows of the large workload (444 vs 455 us).
-template <int VPL>
-__device__ __forceinline__ void store_row16(void* p, u32x4 v) {
-  if constexpr (VPL > 8)
-    st16_stream(p, v);
-  else
-    st16(p, v);
-}
-
 // VPL: 1 KiB segments held per lane-set (row bytes up to VPL KiB per pass).
 // FULL: row bytes == VPL KiB exactly (no per-lane tail test).
 template <int VPL, bool FULL, bool SCALES, int MODE>

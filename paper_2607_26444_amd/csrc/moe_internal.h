@@ -188,6 +188,22 @@ __device__ __forceinline__ u32x4 ld16_stream(const void* p) {
 __device__ __forceinline__ void st16_stream(void* p, u32x4 v) {
   __builtin_nontemporal_store(v, (gu32x4*)(uintptr_t)p);
 }
+// Row stores of the copy kernels (dispatch, expand), VPL KiB per pass:
+// non-temporal for rows of more than 8 KiB, ordinary for narrower rows.
+// Measured in whole steps on MI355X: non-temporal stores are 8-12% faster
+// for dispatch's 14 KiB rows (prefill, decode), ordinary stores 4% faster
+// for the fp8 workload's 7 KiB rows (211 vs 220 us) and 2.5% for the 8 KiB
+// rows of the large workload (444 vs 455 us); in the per-peer chain,
+// ordinary stores made expand 6% faster for those rows (fp8 445 -> 418 us,
+// large 668 -> 635) and the pair dispatch after it 8-10% slower, 0.5% less
+// for the chain.
+template <int VPL>
+__device__ __forceinline__ void store_row16(void* p, u32x4 v) {
+  if constexpr (VPL > 8)
+    st16_stream(p, v);
+  else
+    st16(p, v);
+}
 __device__ __forceinline__ uint32_t ld4(const void* p) { return *(const gu32*)(uintptr_t)p; }
 __device__ __forceinline__ void st4(void* p, uint32_t v) { *(gu32*)(uintptr_t)p = v; }
 
