@@ -489,10 +489,13 @@ int moe_combine_dedup(const uint64_t* partial, int64_t T, int H, int k, int E, i
                       void* stream) {
   if (shape_ok(T, k, E, R)) return MOE_EINVAL;
   const moe::DedupGeom d = moe::dedup_geom(T, k, R);
+  // Sized and split as if every slot were a pair (its parts then count as
+  // large at prefill-sized batches and take the claimed split): on MI355X
+  // 6% faster at prefill and 11% at fp8 than sizing for half the slots,
+  // 2% slower at the large workload, the same at decode.
   return combine_common(partial, nullptr, true, T, H, k, E, R, topk_idx, tok_pos, tok_offset,
                         part_cap, y, workspace, workspace_bytes, d.total, d.g.ticket_offset,
-                        status, MOE_POLICY_BALANCED, 0, nullptr, 0,
-                        (moe::slot_width(k) + 1) / 2, stream);
+                        status, MOE_POLICY_BALANCED, 0, nullptr, 0, moe::slot_width(k), stream);
 }
 
 }  // extern "C"
