@@ -46,14 +46,21 @@
  *  - Device status word `status` (uint32, device): the caller zeroes it;
  *    kernels OR these bits into it and the caller reads it whenever it
  *    synchronizes: MOE_STATUS_BAD_INDEX (an index outside [-1, E): the slot
- *    is treated as unused), MOE_STATUS_DUP_INDEX (an expert repeated within
+ *    is treated as unused; the copy kernels also set it for a slot whose pos
+ *    is set but whose index names no rank -- pos does not belong to
+ *    topk_idx -- and skip that slot), MOE_STATUS_DUP_INDEX (an expert repeated within
  *    one token's row: later repeats are treated as unused),
  *    MOE_STATUS_CAPACITY (a row's region-local index is outside
  *    [0, recv_cap[r]): dispatch does not write it and combine does not read
  *    it; a negative index only arises when pos does not belong to topk_idx),
  *    MOE_STATUS_LAYOUT_SYNC (the layout's workgroups did not all reach its
  *    grid barrier within 2 s -- other work held the compute units that long;
- *    that call's outputs are not valid).
+ *    that call's outputs are not valid: the chunks whose workgroups gave up
+ *    waiting leave their slots unrouted (pos = -1) and parts of the plan
+ *    unwritten, and dispatch and combine still stay inside their buffers --
+ *    they clamp plan ranges to the batch and skip slots whose rank is out of
+ *    range.  The environment variable MOE_LAYOUT_SYNC_LIMIT_US, read once
+ *    per device, replaces the 2 s limit; tests use it to reach this path).
  *  - The three calls of one batch must see the same topk_idx, T, k, E, R and
  *    workspace; dispatch and combine read the partition plan that moe_layout
  *    leaves in the workspace.

@@ -443,6 +443,7 @@ int moe_expand(const uint64_t* dedup_x, const uint64_t* dedup_scales, int dtype,
                                           moe::layout_geom(T, E).ticket_offset) +
               2 * moe::kTicketGroupWords;
   a.status = status;
+  a.R = R;
   return launched(moe::launch_expand(a, as_stream(stream)));
 }
 
@@ -479,6 +480,8 @@ int moe_combine_local(const uint64_t* expert_y, const float* topk_w, int64_t T, 
   a.tok_offset = tok_offset;
   a.bound = static_cast<const int32_t*>(workspace);
   a.status = status;
+  a.tokens = T;
+  a.R = R;
   return launched(moe::launch_combine_local(a, as_stream(stream)));
 }
 

@@ -198,8 +198,13 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
     s_w[wv][kWave + lane] = 0.0f;
   }
 
+  const int T = (int)a.tokens;
   for_each_part<DYN ? kPartsClaimed : kPartsStatic>(a.bound, a.tickets, g, W, lane,
                                                      [&](int t0, int t1) {
+  // token ranges stay inside the batch whatever the plan holds (a layout
+  // whose barrier timed out leaves parts of it unwritten)
+  t0 = max(t0, 0);
+  t1 = min(t1, T);
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t srow = 0;
@@ -209,12 +214,16 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(CombineArgs a) {
       const int p = a.pos[s];
       if (p >= 0) {
         const int r = a.topk_idx[s] / a.L;
-        const int local = p - (DYN ? s_roff[r] : a.rank_offset[r]);
-        if (local >= 0 && local < (DYN ? s_cap[r] : a.recv_cap[r])) {
-          srow = (DYN ? s_ry[r] : a.expert_y[r]) + (uint64_t)local * (uint64_t)rb;
-          wl = a.topk_w ? a.topk_w[s] : 1.0f;   // null: unit weights
+        if ((unsigned)r >= (unsigned)a.R) {
+          st |= MOE_STATUS_BAD_INDEX;   // pos and topk_idx disagree: weight 0
         } else {
-          st |= MOE_STATUS_CAPACITY;
+          const int local = p - (DYN ? s_roff[r] : a.rank_offset[r]);
+          if (local >= 0 && local < (DYN ? s_cap[r] : a.recv_cap[r])) {
+            srow = (DYN ? s_ry[r] : a.expert_y[r]) + (uint64_t)local * (uint64_t)rb;
+            wl = a.topk_w ? a.topk_w[s] : 1.0f;   // null: unit weights
+          } else {
+            st |= MOE_STATUS_CAPACITY;
+          }
         }
       }
     }

@@ -41,6 +41,7 @@ struct ExpandArgs {
   const int32_t* bound;          // plan of the per-slot layout
   uint32_t* tickets;             // claimed parts: {next, done}, zeroed by the layout
   uint32_t* status;
+  int32_t R;                     // ranks
 };
 
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
@@ -61,6 +62,8 @@ struct LocalArgs {
   const int32_t* tok_offset;
   const int32_t* bound;          // plan of the per-slot layout
   uint32_t* status;
+  int64_t tokens;                // T
+  int32_t R;                     // ranks
 };
 
 hipError_t launch_combine_local(const LocalArgs& a, hipStream_t stream);

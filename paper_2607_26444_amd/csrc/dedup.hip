@@ -80,7 +80,11 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
   const bool s16 = SCALES && sb % kVecBytes == 0 && sp % kVecBytes == 0 && sp <= kWaveBytes;
   uint32_t st = 0;
 
+  const int T = (int)a.tokens;
   for_each_part<MODE>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1) {
+  // token ranges stay inside the batch whatever the plan holds
+  t0 = max(t0, 0);
+  t1 = min(t1, T);
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -88,8 +92,13 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(ExpandArgs a) {
       const int64_t s = (int64_t)(tb + lt) * k + lj;
       p = a.pos[s];
       if (p >= 0) {
-        key = a.topk_idx[s] / a.L;
-        q = a.tok_pos[s];
+        const int r = a.topk_idx[s] / a.L;
+        if ((unsigned)r < (unsigned)a.R) {
+          key = r;
+          q = a.tok_pos[s];
+        } else {
+          st |= MOE_STATUS_BAD_INDEX;   // pos and topk_idx disagree: not copied
+        }
       }
     }
     __builtin_amdgcn_wave_barrier();
@@ -264,7 +273,11 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
     s_last[wv][kWave + lane] = 0;
   }
 
+  const int T = (int)a.tokens;
   for_each_part<kPartsStatic>(a.bound, nullptr, g, W, lane, [&](int t0, int t1) {
+  // token ranges stay inside the batch whatever the plan holds
+  t0 = max(t0, 0);
+  t1 = min(t1, T);
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     int key = kNoKey, q = -1, p = -1;
@@ -273,9 +286,14 @@ __global__ __launch_bounds__(kBlock) void combine_local_kernel(LocalArgs a) {
       const int64_t s = (int64_t)(tb + lt) * k + lj;
       p = a.pos[s];
       if (p >= 0) {
-        key = a.topk_idx[s] / a.L;
-        q = a.tok_pos[s];
-        wl = a.topk_w[s];
+        const int r = a.topk_idx[s] / a.L;
+        if ((unsigned)r < (unsigned)a.R) {
+          key = r;
+          q = a.tok_pos[s];
+          wl = a.topk_w[s];
+        } else {
+          st |= MOE_STATUS_BAD_INDEX;   // pos and topk_idx disagree: not combined
+        }
       }
     }
     __builtin_amdgcn_wave_barrier();

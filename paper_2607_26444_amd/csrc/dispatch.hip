@@ -97,7 +97,14 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
     if (s16 && l16 < sb) sv = ld16(a.x_scales + (int64_t)t * sb + l16);
   };
 
+  const int T = (int)a.tokens;
   for_each_part<MODE, true>(a.bound, a.tickets, g, W, lane, [&](int t0, int t1, int next) {
+  // Token ranges (and the token read ahead) stay inside the batch whatever
+  // the plan holds: a layout whose barrier timed out leaves parts of it
+  // unwritten.
+  t0 = max(t0, 0);
+  t1 = min(t1, T);
+  if (next >= T) next = -1;
   for (int tb = t0; tb < t1; tb += tpb) {
     const int te = min(t1, tb + tpb);
     uint64_t dst = 0, sdst = 0;
@@ -106,12 +113,16 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(DispatchArgs a) {
       const int p = a.pos[s];
       if (p >= 0) {
         const int r = a.topk_idx[s] / a.L;
-        const int local = p - s_roff[r];
-        if (local >= 0 && local < s_cap[r]) {
-          dst = s_rx[r] + (uint64_t)local * rb;
-          if (SCALES) sdst = s_rs[r] + (uint64_t)local * sp;
+        if ((unsigned)r >= (unsigned)a.R) {
+          st |= MOE_STATUS_BAD_INDEX;   // pos and topk_idx disagree: not copied
         } else {
-          st |= MOE_STATUS_CAPACITY;
+          const int local = p - s_roff[r];
+          if (local >= 0 && local < s_cap[r]) {
+            dst = s_rx[r] + (uint64_t)local * rb;
+            if (SCALES) sdst = s_rs[r] + (uint64_t)local * sp;
+          } else {
+            st |= MOE_STATUS_CAPACITY;
+          }
         }
       }
     }
@@ -234,6 +245,10 @@ __global__ __launch_bounds__(kBlock) void dispatch_pull_kernel(DispatchArgs a) {
       i1 = b + n * (q + 1) / G;
     }
   }
+  // rows and their sources stay inside the batch whatever the layout left
+  const int64_t n_slots = a.tokens * a.k;
+  i0 = max(i0, (int64_t)0);
+  i1 = min(i1, n_slots);
   uint32_t st = 0;
   for (int64_t ib = i0; ib < i1; ib += kWave) {
     const int64_t ie = min(i1, ib + kWave);
@@ -241,10 +256,13 @@ __global__ __launch_bounds__(kBlock) void dispatch_pull_kernel(DispatchArgs a) {
     if (ib + lane < ie) {
       const int64_t i = ib + lane;
       const int s = a.row_src[i];
-      const int t = s / a.k;
-      const int r = a.topk_idx[s] / a.L;
-      const int64_t local = i - a.rank_offset[r];
-      if (local >= 0 && local < a.recv_cap[r]) {
+      const bool known = s >= 0 && s < n_slots;
+      const int t = known ? s / a.k : 0;
+      const int r = known ? a.topk_idx[s] / a.L : -1;
+      const int64_t local = (unsigned)r < (unsigned)a.R ? i - a.rank_offset[r] : -1;
+      if (!known || (unsigned)r >= (unsigned)a.R) {
+        st |= MOE_STATUS_BAD_INDEX;
+      } else if (local >= 0 && local < a.recv_cap[r]) {
         src = reinterpret_cast<uint64_t>(a.x) + (uint64_t)t * rb;
         dst = a.recv_x[r] + (uint64_t)local * rb;
         if (SCALES) {

@@ -37,6 +37,7 @@
 // out one row per (token, peer) pair: E is then the number of peers and
 // load_row bins the expert indices by peer as it reads them.
 
+#include <cstdlib>
 #include <map>
 #include <mutex>
 #include <tuple>
@@ -370,6 +371,7 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
     __syncthreads();
   }
   if constexpr (MODE == kPlaceFused) {
+    __shared__ uint32_t s_late;   // this workgroup's wait timed out
     // Publish this chunk's count row, then wait for every chunk's (wave 0
     // alone: one flag per workgroup).
     if (w == 0) {
@@ -407,12 +409,27 @@ __global__ __launch_bounds__(kBlock) void layout_place_kernel(
         __builtin_amdgcn_s_sleep(1);
       }
       // every workgroup read the generation before it published its flag
+      // (advanced after a time-out too, so no flag of this call can pass the
+      // next call's barrier)
       if (c == 0 && lane == 0)
         __hip_atomic_store(gen, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (lane == 0) s_late = (st & MOE_STATUS_LAYOUT_SYNC) ? 1u : 0u;
     }
     // Every wave reads the count matrix after this point, with coherent
     // loads (below).
     __syncthreads();
+    if (s_late) {
+      // Some chunk's counts did not arrive in time: this chunk places
+      // nothing.  Its slots are marked unrouted, so the copy kernels skip
+      // them, and the status word carries MOE_STATUS_LAYOUT_SYNC; every
+      // workgroup that saw all flags places its chunk from complete counts.
+      for (int64_t i = c0 * k + tid; i < c1 * k; i += kBlock) pos[i] = -1;
+      if (c == 0 && tid < kTicketGroups * 16 * 2)   // the copy kernels' tickets, as below
+        tickets[(tid >> 1) * kTicketStride + (tid & 1)] = 0u;
+      st = wave_or(st);
+      if (lane == 0 && st) atomicOr(status, st);
+      return;
+    }
   }
   if (SINGLE) {
 #pragma unroll
@@ -674,8 +691,10 @@ int resident_blocks(const void* kernel, size_t lds_bytes) {
   return cache[key] = cus * blocks;
 }
 
-// Time limit of the fused layout's grid barrier in wall-clock ticks (2 s),
-// from the current device's wall-clock rate (queried once per device).
+// Time limit of the fused layout's grid barrier in wall-clock ticks: 2 s,
+// or MOE_LAYOUT_SYNC_LIMIT_US microseconds when that environment variable is
+// set (tests of the time-out path), at the current device's wall-clock rate
+// (read once per device).
 uint64_t sync_limit_ticks() {
   static std::mutex mu;
   static std::map<int, uint64_t> cache;
@@ -688,7 +707,13 @@ uint64_t sync_limit_ticks() {
   if (dev < 0 || hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
       khz < 1)
     khz = 100000;
-  return cache[dev] = (uint64_t)khz * 2000u;
+  uint64_t us = 2000000u;
+  if (const char* e = std::getenv("MOE_LAYOUT_SYNC_LIMIT_US")) {
+    char* end = nullptr;
+    const unsigned long long v = std::strtoull(e, &end, 10);
+    if (end != e && v <= 60000000ull) us = v;
+  }
+  return cache[dev] = (uint64_t)khz * us / 1000u;
 }
 
 template <int KW, bool FIXED>

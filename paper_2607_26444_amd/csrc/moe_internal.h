@@ -343,11 +343,17 @@ __device__ __forceinline__ void for_each_part(const int32_t* bound, uint32_t* ti
   const int shards = ticket_shards(W);
   const int shard = ticket_shard(g, W);
   uint32_t* next_claim = tickets + shard * kTicketStride;
+  // claims past the last part end the loop (unsigned: a counter that was
+  // never reset cannot produce a negative part)
+  const int span = MOE_PLAN_PARTS - first;
+  const uint32_t n_claims = span > 0 ? (uint32_t)((span + G - 1) / G) : 0u;
   for (;;) {
-    int t = 0;
-    if (lane == 0) t = (int)atomicAdd(next_claim, 1u);
-    const int p0 = first + (__builtin_amdgcn_readfirstlane(t) * shards + shard) * G;
-    if (p0 >= MOE_PLAN_PARTS) break;
+    uint32_t t = 0;
+    if (lane == 0) t = atomicAdd(next_claim, 1u);
+    const uint32_t claim =
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)t) * (uint32_t)shards + (uint32_t)shard;
+    if (claim >= n_claims) break;
+    const int p0 = first + (int)claim * G;
     int b0 = 0, b1 = 0;
     if (lane < G && p0 + lane < MOE_PLAN_PARTS) {
       b0 = (int)ld4(bound + p0 + lane);

@@ -216,3 +216,105 @@ def test_layout_with_index_rows_off_16_byte_alignment(T, E, R, k):
     lay = moe.Layout(T, k, E, R)
     lay.run(view)
     _check(lay, idx, E, R, what=f"offset T={T} k={k}")
+
+
+_TIME_OUT_CHILD = r'''
+import sys
+import numpy as np
+import torch
+import gpu_harness as h
+import workloads as wl
+from paper_2607_26444_amd import moe
+
+T, H, E, R, k = 32768, 512, 256, 64, 8      # 128 chunks: the one-launch form
+CHUNK = 256
+cfg = wl.custom(T, H, E, R, k, seed=77)
+inp = wl.make_inputs(cfg)
+ref = h.oracle_chain(cfg, inp)
+lay_ref = ref["layout"]
+rows = [max(1, int(c)) for c in lay_ref["rank_count"]]
+rb = 2 * H
+x_d = h.to_dev(h.u8_rows(inp["x"]))
+idx_d = h.to_dev(inp["topk_idx"])
+w_d = h.to_dev(inp["topk_w"])
+lay = moe.Layout(T, k, E, R)
+regions = moe.Regions(rows, rb, guard_bytes=h.GUARD, fill=h.SENTINEL)
+eregions = moe.Regions(rows, rb, guard_bytes=h.GUARD, fill=h.SENTINEL)
+for r in range(R):
+    n = int(lay_ref["rank_count"][r])
+    if n:
+        eregions.region(r)[:n].copy_(h.to_dev(ref["ey"][r].view(np.uint8).reshape(n, rb)))
+cap_d = h.to_dev(np.asarray(rows, dtype=np.int32))
+# rank offsets as a previous call with this routing leaves them: the first
+# workgroup writes them, and may give up waiting before it does
+lay.rank_offset.copy_(h.to_dev(lay_ref["rank_offset"].astype(np.int32)))
+pos_ref = lay_ref["pos"].reshape(-1, CHUNK * k)
+y_ref = ref["y"].reshape(T, H)
+late_calls = 0
+for call in range(6):
+    print("[child] call", call, flush=True)
+    regions.buf.fill_(h.SENTINEL)
+    y = torch.full((T, H), 0x5A5A, dtype=torch.int16, device="cuda")
+    lay.status.zero_()
+    lay.run(idx_d)
+    moe.moe_dispatch(x_d, None, moe.MOE_DTYPE_BF16, H, E, R, idx_d, lay.pos, lay.rank_offset,
+                     regions.table, None, cap_d, lay.workspace, lay.status)
+    moe.moe_combine(eregions.table, w_d, H, E, R, idx_d, lay.pos, lay.rank_offset, cap_d, y,
+                    lay.workspace, lay.status)
+    torch.cuda.synchronize()
+    st = int(lay.status.item())
+    pos = lay.pos.cpu().numpy()[:T * k].reshape(-1, CHUNK * k)
+    late = np.array([bool((p == -1).all()) for p in pos])
+    for c in range(len(pos)):
+        assert late[c] or np.array_equal(pos[c], pos_ref[c]), ("chunk misplaced", call, c)
+    if st & moe.MOE_STATUS_LAYOUT_SYNC:
+        late_calls += 1
+    else:
+        assert not late.any(), ("chunks unrouted without the status bit", call)
+    # regions: every row is untouched or the oracle's; nothing outside them
+    buf = regions.buf.cpu().numpy()
+    inside = np.zeros(buf.shape[0], bool)
+    for r, off in enumerate(regions.offsets):
+        got = buf[off: off + rows[r] * rb].reshape(rows[r], rb)
+        want = ref["regs"][r]
+        n = want.shape[0]
+        untouched = (got == h.SENTINEL).all(1)
+        assert np.all(untouched[n:]), ("row past the routed rows written", call, r)
+        assert np.all(untouched[:n] | (got[:n] == want).all(1)), ("wrong row", call, r)
+        inside[off: off + rows[r] * rb] = True
+    assert np.all(buf[~inside] == h.SENTINEL), ("bytes outside the regions", call)
+    # y: each row untouched, zero (a token left unrouted) or the oracle's
+    yy = y.cpu().numpy().view(np.uint16)
+    untouched = (yy == 0x5A5A).all(1)
+    zero = (yy == 0).all(1)
+    rest = ~(untouched | zero)
+    assert not np.any(zero & ~np.repeat(late, CHUNK)), ("zero row of a placed chunk", call)
+    ok, msg = h.combine_close(yy[rest], y_ref[rest])
+    assert ok, (call, msg)
+    print("[child] call", call, "status", st, "unrouted chunks", int(late.sum()), flush=True)
+print("ok", late_calls, flush=True)
+'''
+
+
+def test_barrier_time_out_keeps_every_write_in_bounds():
+    """The barrier's time limit forced to zero from the host
+    (MOE_LAYOUT_SYNC_LIMIT_US=0, in a child process, so that the limit holds
+    from the library's first launch): a workgroup that does not see every
+    flag at its first look gives up.  Its chunk's slots come back unrouted,
+    every other chunk's positions equal the oracle's, the status word says
+    MOE_STATUS_LAYOUT_SYNC, and dispatch and combine, run on whatever the
+    layout left (parts of the plan unwritten), write only rows the oracle
+    has and nothing outside their buffers."""
+    import os
+    import subprocess
+    import sys
+    here = os.path.dirname(os.path.abspath(__file__))
+    env = dict(os.environ, MOE_LAYOUT_SYNC_LIMIT_US="0",
+               PYTHONPATH=os.pathsep.join([os.path.dirname(here), here,
+                                           os.environ.get("PYTHONPATH", "")]))
+    r = subprocess.run([sys.executable, "-u", "-c", _TIME_OUT_CHILD], env=env,
+                       capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, (r.stdout[-3000:], r.stderr[-3000:])
+    last = r.stdout.strip().splitlines()[-1]
+    assert last.startswith("ok"), r.stdout[-3000:]
+    print(r.stdout[-2000:])
