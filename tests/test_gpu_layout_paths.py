@@ -115,7 +115,8 @@ def test_layout_forms_match_oracle(T, E, R, k, zipf, mask):
 
 
 @pytest.mark.parametrize("T,E,R,k,C", [(4096, 256, 64, 8, 160), (40000, 256, 64, 8, 1400),
-                                       (1000, 16, 4, 4, 200)])
+                                       (1000, 16, 4, 4, 200),
+                                       (32768, 256, 64, 8, 900)])   # one launch, 128 chunks
 def test_fixed_capacity_forms_match_oracle(T, E, R, k, C):
     from paper_2607_26444_amd import moe
     idx = _routing(T, k, E, seed=T + C, zipf=1.2)
