@@ -230,3 +230,45 @@ def test_layout_scratch_array_covers_every_shape():
     for T in (0, 1, 255, 256, 257, 4096, 16384, 2 ** 20):
         for E in (1, 3, 16, 256, 1024):
             assert moe.moe_layout_workspace_bytes(T, 1, E, 1) <= 576 * 1024
+
+
+_C_CLIENT = r"""
+#include <stdio.h>
+#include <string.h>
+#include "moe.h"
+
+int main(void) {
+  size_t bytes = 0;
+  if (moe_version() != MOE_VERSION) return 1;
+  if (strcmp(moe_strerror(MOE_OK), "ok") != 0) return 2;
+  if (moe_layout_workspace_bytes(16384, 8, 256, 64, &bytes) != MOE_OK) return 3;
+  if (bytes < (size_t)(MOE_PLAN_PARTS + 1) * 4) return 4;
+  if (moe_layout_workspace_bytes(16, 0, 256, 64, &bytes) != MOE_EINVAL) return 5;
+  printf("%zu\n", bytes);
+  return 0;
+}
+"""
+
+
+def test_header_builds_a_c_program_that_links_the_library(tmp_path):
+    """include/moe.h is a plain C header: a C99 program that includes it
+    builds with every warning as an error, links libmoe.so and calls its
+    host-side entry points (version, error text, workspace query)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    moe.lib()
+    src = tmp_path / "client.c"
+    src.write_text(_C_CLIENT)
+    exe = tmp_path / "client"
+    libdir = os.path.dirname(moe.LIB_PATH)
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-I",
+                        os.path.join(ROOT, "include"), str(src), "-o", str(exe), "-L", libdir,
+                        "-l:libmoe.so", "-Wl,-rpath," + libdir],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert run.returncode == 0, (run.returncode, run.stderr)
+    assert int(run.stdout.strip()) == moe.moe_layout_workspace_bytes(16384, 8, 256, 64)
