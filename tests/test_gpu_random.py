@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 # MOE_RANDOM_CASES=n widens a run to n per-slot and n/2 deduplicated cases.
-N_SLOT_CASES = int(os.environ.get("MOE_RANDOM_CASES", "48"))
+N_SLOT_CASES = int(os.environ.get("MOE_RANDOM_CASES", "96"))
 N_DEDUP_CASES = N_SLOT_CASES // 2
 BUDGET = 40_000_000   # T * k * H per case (row bytes the oracle and checks touch)
 
